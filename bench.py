@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark: diagonal-aware sparse vs dense on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step is one decode step of the whole hot path over every layer of the
+workload: ``dsa_plan -> dsa_decode_attention (split-K + combine) ->
+dsa_select`` per layer, all inputs resident in HBM.  The dense mode of the
+same kernels, on the same inputs and positions, is timed alongside for the
+speedup.  Prints one JSON line.
+
+``roofline`` describes the decode kernel (the dominant one): algorithmic K/V
+bytes per launch (4*d bytes per attended key per KV head) divided by its
+mean launch time from HIP events recorded around every launch inside the
+timed steps.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
+of the same workload (``--no-cpu-baseline`` skips it).
+"""
+
+from __future__ import annotations
+
+import argparse
+import copy
+import hashlib
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBPS = 8000.0
+METRIC = "decode attention tokens/s + KV HBM GB/s (% of 8 TB/s), speedup vs dense"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llamagen_xl")
+    ap.add_argument("--positions", default=None, help="ragged | last | first")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in ("decode.hip", "device.h", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_19702_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(workload, src_hash):
+    """HBM bytes per decode launch from committed rocprofv3 counter runs, if
+    they were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(workload)
+    if not ent or ent.get("kernel_hash") != src_hash:
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(bt, seconds):
+    """The fp64 oracle on a bounded sample: a few requests of layer 0, each
+    decode step repeated until about ``seconds`` of CPU time is spent."""
+    import numpy as np
+    import torch
+    from oracle import step as ostep
+    from paper_2609_19702_amd import synth
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    w, L = bt.w, bt.layers[0]
+    order = sorted(range(w.batch), key=lambda b: bt.pos_host[b])
+    pick = [order[i * (len(order) - 1) // 5] for i in range(6)]
+    units = []
+    qn = L.q.to(torch.float64).cpu().numpy()
+    for b in pick:
+        t = bt.pos_host[b]
+        k = L.kv.k[b].to(torch.float64).cpu().numpy()
+        v = L.kv.v[b].to(torch.float64).cpu().numpy()
+        ints = synth.random_ints(w, 0, w.num_kv_heads * w.window, sub=b).tolist()
+        st = ostep.random_states(w.num_kv_heads, bt.p.window, bt.p.n_att, t, ints)
+        units.append((t, qn[b], k[:, :w.prompt_len], v[:, :w.prompt_len],
+                      k[:, w.prompt_len:], v[:, w.prompt_len:], st))
+    ctx = threadpool_limits(1) if threadpool_limits else None
+    done, spent = 0, 0.0
+    try:
+        while spent < seconds:
+            for (t, q, Kp, Vp, K, V, st) in units:
+                st2 = copy.deepcopy(st)
+                t0 = time.perf_counter()
+                ostep.request_step(t, q, Kp, Vp, K, V, bt.scale, "diagonal", st2)
+                spent += time.perf_counter() - t0
+                done += 1
+    finally:
+        if ctx is not None:
+            ctx.__exit__(None, None, None)
+    tok_s = done / spent / len(bt.layers)
+    return {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{len(units)} requests of layer 0 (positions "
+                       f"{[bt.pos_host[b] for b in pick]}), one decode step each (attention "
+                       f"for all {w.num_q_heads} heads + selection), repeated {done} times in "
+                       f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
+
+
+def timed(bt, steps, dense):
+    import torch
+    from paper_2609_19702_amd import workload
+    n = len(bt.layers)
+    timers = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)] for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(steps):
+        workload.step(bt, dense=dense, timers=timers[k])
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / steps
+    launch = [a.elapsed_time(b) for row in timers for (a, b) in row]
+    return ms, launch
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the decode path has no "
+              "cross-GPU step: requests and heads shard with no exchange", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2609_19702_amd import synth, workload
+    from paper_2609_19702_amd import binding as B
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    w = synth.WORKLOADS[args.workload]
+    if args.positions:
+        w = w.with_(positions=args.positions)
+    t0 = time.time()
+    bt = workload.make_batch(w)
+    workload.build_histories(bt)
+    torch.cuda.synchronize()
+    print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
+          f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        workload.step(bt, dense=False)
+        workload.step(bt, dense=True)
+    torch.cuda.synchronize()
+    ms_sparse, launch_sparse = timed(bt, args.steps, dense=False)
+    ms_dense, launch_dense = timed(bt, args.steps, dense=True)
+    print(f"# sparse {ms_sparse:.3f} ms/step, dense {ms_dense:.3f} ms/step", file=sys.stderr, flush=True)
+
+    n_layers = len(bt.layers)
+    bytes_sparse = bt.kv_bytes(dense=False)
+    bytes_dense = bt.kv_bytes(dense=True)
+    per_launch = bytes_sparse / n_layers
+    mean_launch_ms = statistics.fmean(launch_sparse)
+    achieved = per_launch / (mean_launch_ms * 1e-3) / 1e9
+    dense_launch_ms = statistics.fmean(launch_dense)
+    info = B.launch_info(bt.p, bt.s)
+    src_hash = kernel_source_hash()
+    traffic = traffic_for(w.name, src_hash)
+
+    base = None
+    if not args.no_cpu_baseline:
+        base = cpu_baseline(bt, args.cpu_seconds)
+
+    res = {
+        "metric": METRIC,
+        "value": w.batch / (ms_sparse * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_sparse,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{w.name}_like", "layers": n_layers, "batch": w.batch,
+            "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
+            "prompt_len": w.prompt_len, "grid": f"{w.grid_h}x{w.grid_w}", "window": bt.p.window,
+            "n_att": bt.p.n_att, "sparsity": round(1 - bt.p.n_att / w.decode_len, 4),
+            "positions": w.positions, "accumulate": "fp32",
+            "splits": info.max_splits, "rows_per_split": info.rows_per_split,
+        },
+        "kv_gbps": bytes_sparse / (ms_sparse * 1e-3) / 1e9,
+        "kv_hbm_frac": bytes_sparse / (ms_sparse * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "dense": {
+            "ms_per_step": ms_dense, "tokens_per_s": w.batch / (ms_dense * 1e-3),
+            "kv_gbps": bytes_dense / (ms_dense * 1e-3) / 1e9,
+            "decode_launch_us": dense_launch_ms * 1e3,
+            "decode_launch_gbps": bytes_dense / n_layers / (dense_launch_ms * 1e-3) / 1e9,
+        },
+        "speedup_vs_dense": ms_dense / ms_sparse,
+        "ideal_speedup": bytes_dense / bytes_sparse,
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
+            "kernel": "decode_kernel (+ combine when split)", "bytes_per_launch": per_launch,
+            "launch_us": mean_launch_ms * 1e3, "source_hash": src_hash,
+        },
+        "cpu_baseline": base,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,286 @@
+/*
+ * dsa.h -- diagonal-aware sparse decode attention on AMD Instinct MI355X
+ * (gfx950): the C ABI of libdsa.so.
+ *
+ * The library computes the decode-phase attention of an autoregressive
+ * image generator with the kept-KV selection of Algorithm 1 of the paper
+ * (section 4, "Diagonal-Aware Sparse Attention"):
+ *
+ *   - the prompt KV (L_p rows) is always attended in full;
+ *   - inside a recent window of N_r decode positions, a per-head list of
+ *     skipped entries grows by one per step during phase 2 (an argmin of the
+ *     window softmax) and then stays fixed; because both the list entries and
+ *     the step index advance by +1 per step, every entry is stored as its
+ *     relative offset d = t - j, which never changes, so the per-step "shift"
+ *     of the algorithm costs nothing;
+ *   - each step attends exactly min(t + 1, N_att) decode rows;
+ *   - a dense mode (all decode rows 0 .. t) is the baseline the paper
+ *     compares against in its evaluation (section 5).
+ *
+ * A decode step for one layer is:
+ *
+ *     dsa_plan              kept decode positions per (request, KV head)
+ *     dsa_decode_attention  split-K attention over prompt + kept rows, then
+ *                           the cross-split log-sum-exp combine
+ *     dsa_select            phase-2 argmin, appends one offset per KV head
+ *
+ * Conventions for every call:
+ *   - Pointers named d_* are DEVICE pointers owned by the caller.  The
+ *     library never allocates device memory and keeps no device state between
+ *     calls; buffer sizes come from the *_bytes queries.
+ *   - Calls that take a hipStream_t only enqueue work on that stream and
+ *     return without synchronising; results are visible to later work on the
+ *     same stream.  Calls on distinct buffers may run concurrently.
+ *   - Every entry point returns a dsa_status; no C++ exception crosses the
+ *     ABI.  Arguments are validated on the host before anything is enqueued.
+ *   - Device-side precondition failures (a decode position outside the grid,
+ *     a corrupt selection state) never cause an out-of-bounds access: the
+ *     value is clamped or ignored and a bit is set in the per-(request, KV
+ *     head) flag words of the plan or state buffer.
+ *   - Query head h reads KV head h / (num_q_heads / num_kv_heads).
+ *   - "bf16" is IEEE bfloat16; "fp32" is IEEE binary32.
+ */
+#ifndef DSA_H_
+#define DSA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DSA_API __attribute__((visibility("default")))
+
+#define DSA_ABI_VERSION 1
+
+/* ---- status codes -------------------------------------------------------- */
+typedef int32_t dsa_status;
+#define DSA_OK               0
+#define DSA_ERR_INVALID_ARG (-1) /* a NULL pointer or an out-of-range value */
+#define DSA_ERR_UNSUPPORTED (-2) /* valid but not built: head_dim, group size */
+#define DSA_ERR_WORKSPACE   (-3) /* a caller buffer is smaller than required */
+#define DSA_ERR_HIP         (-4) /* the HIP runtime refused a launch */
+
+/* ---- modes ----------------------------------------------------------------- */
+#define DSA_MODE_DENSE    0 /* attend prompt + decode rows 0 .. t            */
+#define DSA_MODE_DIAGONAL 1 /* attend prompt + the rows Algorithm 1 keeps     */
+
+/* ---- per-(request, KV head) flag bits (plan and state buffers) ------------ */
+#define DSA_FLAG_INACTIVE      1  /* decode position < 0: request slot unused   */
+#define DSA_FLAG_POS_CLAMPED   2  /* decode position >= H*W, clamped to H*W-1   */
+#define DSA_FLAG_STATE_BEHIND  4  /* fewer skip entries than the step needs     */
+#define DSA_FLAG_BAD_OFFSET    8  /* a stored offset outside [0, N_r-2] ignored */
+#define DSA_FLAG_COUNT         16 /* kept count differs from min(t+1, N_att)    */
+
+/*
+ * Method parameters (Algorithm 1 inputs, section 4).
+ *   prompt_len  L_p >= 0, prompt rows always attended
+ *   grid_h/w    visual token grid, >= 1; L_dec = grid_h * grid_w decode steps
+ *   window      N_r, recent window, 1 <= N_r <= 65535
+ *   n_att       N_att, decode rows attended per step, 1 <= N_att <= N_r
+ *   mode        DSA_MODE_DENSE or DSA_MODE_DIAGONAL
+ */
+typedef struct dsa_params {
+  int32_t prompt_len;
+  int32_t grid_h;
+  int32_t grid_w;
+  int32_t window;
+  int32_t n_att;
+  int32_t mode;
+} dsa_params;
+
+/*
+ * Problem shape of one layer.
+ *   batch        B >= 1 requests
+ *   num_q_heads  Hq >= 1
+ *   num_kv_heads Hkv >= 1, Hq % Hkv == 0, group Hq / Hkv in {1, 2, 4, 8}
+ *   head_dim     d in {64, 128}
+ */
+typedef struct dsa_shape {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+} dsa_shape;
+
+/*
+ * Where row r of KV head h of request b lives in the K and V arrays (both
+ * arrays share one layout).  Rows 0 .. L_p-1 are the prompt; decode position
+ * j is row L_p + j.  Element offset of the row's first element:
+ *     base(b) + h * stride_head + r * stride_row
+ * with base(b) = d_row_base[b] when d_row_base is non-NULL (a device array of
+ * B int64 values, e.g. for ragged packing), else b * stride_batch.
+ * A row holds head_dim contiguous bf16 values.  The K/V base pointers and
+ * every base(b), stride_head and stride_row must be multiples of 8 elements
+ * (16 bytes).  The caller guarantees every row up to L_p + t_b exists.
+ */
+typedef struct dsa_kv_layout {
+  const int64_t* d_row_base;
+  int64_t stride_batch;
+  int64_t stride_head;
+  int64_t stride_row;
+} dsa_kv_layout;
+
+/* Byte offsets of the arrays inside a plan buffer (all int32):
+ *   count  [B*Hkv]           kept decode rows of (b, h), index b*Hkv + h
+ *   flags  [B*Hkv]           DSA_FLAG_* bits
+ *   indices[B*Hkv][cap]      kept decode positions of (b, h), ascending
+ * cap = min(N_att, L_dec) in diagonal mode and 0 in dense mode.           */
+typedef struct dsa_plan_layout {
+  size_t count_offset;
+  size_t flags_offset;
+  size_t indices_offset;
+  int32_t cap;
+  size_t bytes;
+} dsa_plan_layout;
+
+/* Byte offsets of the arrays inside a selection-state buffer:
+ *   count   int32  [B*Hkv]        skip entries stored for (b, h)
+ *   flags   int32  [B*Hkv]        DSA_FLAG_* bits set by dsa_select
+ *   offsets uint16 [B*Hkv][cap]   skip entries as offsets d = t - j, in the
+ *                                 order Algorithm 1 appends them
+ * cap = N_r - N_att (the largest skip list of Algorithm 1).               */
+typedef struct dsa_state_layout {
+  size_t count_offset;
+  size_t flags_offset;
+  size_t offsets_offset;
+  int32_t cap;
+  size_t bytes;
+} dsa_state_layout;
+
+/* How dsa_decode_attention splits the keys (for reports and tests). */
+typedef struct dsa_launch_info {
+  int32_t rows_per_split;  /* C: keys per split workgroup                   */
+  int32_t max_splits;      /* S: splits per (request, KV head) at most      */
+  int32_t workgroups;      /* B * Hkv * S                                   */
+  int32_t kernel_variant;  /* implementation variant id                     */
+  size_t workspace_bytes;  /* fp32 partials for the combine                 */
+} dsa_launch_info;
+
+/* ---- host-only helpers (no device work) ---------------------------------- */
+
+/* ABI version (DSA_ABI_VERSION of the built library). */
+DSA_API int32_t dsa_abi_version(void);
+
+/* Human-readable message for a status code; never NULL. */
+DSA_API const char* dsa_status_str(dsa_status status);
+
+/*
+ * Fill *out from a target sparsity (section 5.1: sparsity = 1 - N_att/L_dec)
+ * and the window rule of the "Parameter selection" paragraph of section 4.
+ *   window = 0 selects the paper's default N_r = L_dec / 2 (at least 1);
+ *   n_att = clamp(floor((1000 - sparsity_permille) * L_dec / 1000 + 1/2),
+ *                 1, N_r), computed in integers.
+ * Errors: DSA_ERR_INVALID_ARG for out == NULL, sparsity outside [0, 1000],
+ * negative prompt_len, grid < 1, window outside [0, 65535] or a bad mode.
+ */
+DSA_API dsa_status dsa_params_from_sparsity(int32_t prompt_len, int32_t grid_h, int32_t grid_w,
+                                            int32_t window, int32_t sparsity_permille,
+                                            int32_t mode, dsa_params* out);
+
+/* Validate a parameter/shape pair as every device call does.  Returns
+ * DSA_OK, DSA_ERR_INVALID_ARG or DSA_ERR_UNSUPPORTED. */
+DSA_API dsa_status dsa_validate(const dsa_params* p, const dsa_shape* s);
+
+/* Buffer layouts; *out is filled only on DSA_OK. */
+DSA_API dsa_status dsa_get_state_layout(const dsa_params* p, const dsa_shape* s,
+                                        dsa_state_layout* out);
+DSA_API dsa_status dsa_get_plan_layout(const dsa_params* p, const dsa_shape* s,
+                                       dsa_plan_layout* out);
+DSA_API dsa_status dsa_get_launch_info(const dsa_params* p, const dsa_shape* s,
+                                       dsa_launch_info* out);
+
+/* Sizes in bytes (0 when p/s are invalid). */
+DSA_API size_t dsa_state_bytes(const dsa_params* p, const dsa_shape* s);
+DSA_API size_t dsa_plan_bytes(const dsa_params* p, const dsa_shape* s);
+DSA_API size_t dsa_workspace_bytes(const dsa_params* p, const dsa_shape* s);
+/* Number of fp32 window logits per call: B * Hq * cap (plan cap). */
+DSA_API size_t dsa_window_logits_count(const dsa_params* p, const dsa_shape* s);
+
+/* ---- device calls ---------------------------------------------------------- */
+
+/*
+ * Empty the skip lists of the selected requests: Algorithm 1 starts every
+ * request with skip_idx = [].  Clears count and flags of (b, h) for every KV
+ * head h of each request b with d_req_mask[b] != 0 (every request when
+ * d_req_mask is NULL).  d_state: state buffer of dsa_state_bytes bytes.
+ * Uses a kernel, never a memset, so it may be captured in a HIP graph.
+ */
+DSA_API dsa_status dsa_state_reset(const dsa_params* p, const dsa_shape* s, void* d_state,
+                                   const int32_t* d_req_mask, hipStream_t stream);
+
+/*
+ * Kept decode positions of one step (Algorithm 1: "window - skip_idx" with
+ * window = [max(0, t-N_r), .., t] and K[t-N_r] evicted in phase 3).
+ *   d_decode_pos  int32 [B]: t_b, the newest decode position of request b
+ *                 (its K/V row L_p + t_b is already written); t_b < 0 marks
+ *                 an unused slot (count 0, output zeros).
+ *   d_state       selection state; the step uses the first
+ *                 clamp(t_b - N_att + 1, 0, N_r - N_att) entries of each list
+ *                 (the entries appended at steps < t_b), so replaying a step
+ *                 is exact.  Ignored (may be NULL) in dense mode.
+ *   d_plan        output, plan_bytes >= dsa_plan_bytes().  For each (b, h):
+ *                 count = kept rows (diagonal: min(t_b+1, N_att)), flags,
+ *                 and in diagonal mode the kept positions t_b - d for offsets
+ *                 d in [0, min(t_b, N_r-1)] not in the skip list, ascending.
+ * Errors: INVALID_ARG (NULL pointers, bad params), UNSUPPORTED, WORKSPACE
+ * (plan_bytes too small), HIP.
+ */
+DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,
+                            const void* d_state, void* d_plan, size_t plan_bytes,
+                            hipStream_t stream);
+
+/*
+ * Attn(Q_t, K_p + K[idx], V_p + V[idx]) of Algorithm 1 for every request and
+ * query head: softmax(sm_scale * q . k) over the prompt rows plus the kept
+ * decode rows of the plan (diagonal mode) or all decode rows 0 .. t_b (dense
+ * mode), times V.  Keys are split into chunks processed by independent
+ * workgroups with an fp32 online softmax; a second kernel merges the chunks
+ * by log-sum-exp when a request has more than one.
+ *   d_q              bf16 [B][Hq][d]
+ *   d_k, d_v         bf16 caches in the dsa_kv_layout layout
+ *   d_decode_pos     int32 [B] as for dsa_plan
+ *   d_plan           plan of the same step (diagonal mode); may be NULL in
+ *                    dense mode
+ *   sm_scale         softmax scale, normally 1/sqrt(d)
+ *   d_out            fp32 [B][Hq][d]; zeros for unused slots
+ *   d_window_logits  NULL, or fp32 [B][Hq][cap]: sm_scale * q . k of every
+ *                    kept decode row in plan order (diagonal mode; entries
+ *                    past count are not written).  dsa_select reads them.
+ *   d_ws, ws_bytes   workspace of at least dsa_workspace_bytes() bytes
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
+ */
+DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                        const void* d_k, const void* d_v,
+                                        const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                        const void* d_plan, float sm_scale, float* d_out,
+                                        float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                        hipStream_t stream);
+
+/*
+ * Phase-2 selection of Algorithm 1: for every request with
+ * N_att - 1 <= t_b <= N_r - 2 and every KV head h, compute
+ *   w_q = softmax(window logits of query head q)   over the kept window
+ *   sigma_j = sum of w_q[j] over the query heads q that read KV head h
+ *   j* = argmin_j sigma_j (first, i.e. oldest, on ties)
+ * and store offset t_b - idx[j*] as skip entry number k = t_b - N_att + 1
+ * (count becomes k + 1).  At group size 1 the argmin is taken on the logits,
+ * which orders exactly as the softmax.  Requests outside that step range, and
+ * dense mode, are left untouched.  A state with fewer than k entries is left
+ * unchanged and flagged DSA_FLAG_STATE_BEHIND.
+ *   d_plan, d_window_logits  from dsa_plan / dsa_decode_attention of this step
+ *   d_state                  in/out
+ * Errors: INVALID_ARG, UNSUPPORTED, HIP.
+ */
+DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,
+                              const void* d_plan, const float* d_window_logits, void* d_state,
+                              hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSA_H_ */

@@ -1,0 +1,339 @@
+// Host side of the C ABI: argument validation, buffer layouts, the split
+// configuration of the decode kernel, and the extern "C" entry points.
+#include <cmath>
+#include <cstdlib>
+
+#include "internal.h"
+
+namespace dsa {
+namespace {
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int env_int(const char* name, int fallback) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return fallback;
+  char* end = nullptr;
+  long x = std::strtol(v, &end, 10);
+  return (end && *end == 0 && x > 0 && x < (1 << 20)) ? static_cast<int>(x) : fallback;
+}
+
+}  // namespace
+
+dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
+  if (!p || !s || !d) return DSA_ERR_INVALID_ARG;
+  if (p->prompt_len < 0 || p->grid_h < 1 || p->grid_w < 1) return DSA_ERR_INVALID_ARG;
+  if (p->mode != DSA_MODE_DENSE && p->mode != DSA_MODE_DIAGONAL) return DSA_ERR_INVALID_ARG;
+  if (p->window < 1 || p->window > 65535) return DSA_ERR_INVALID_ARG;
+  if (p->n_att < 1 || p->n_att > p->window) return DSA_ERR_INVALID_ARG;
+  const int64_t ldec = static_cast<int64_t>(p->grid_h) * p->grid_w;
+  if (ldec > (1 << 24) || p->prompt_len > (1 << 24)) return DSA_ERR_INVALID_ARG;
+  if (s->batch < 1 || s->num_q_heads < 1 || s->num_kv_heads < 1) return DSA_ERR_INVALID_ARG;
+  if (s->num_q_heads % s->num_kv_heads) return DSA_ERR_INVALID_ARG;
+  if (s->head_dim != 64 && s->head_dim != 128) return DSA_ERR_UNSUPPORTED;
+  const int G = s->num_q_heads / s->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return DSA_ERR_UNSUPPORTED;
+  const int64_t pairs = static_cast<int64_t>(s->batch) * s->num_kv_heads;
+  if (pairs * s->num_q_heads / s->num_kv_heads * s->head_dim > (int64_t(1) << 31))
+    return DSA_ERR_INVALID_ARG;
+
+  d->B = s->batch;
+  d->Hq = s->num_q_heads;
+  d->Hkv = s->num_kv_heads;
+  d->G = G;
+  d->D = s->head_dim;
+  d->Lp = p->prompt_len;
+  d->Ldec = static_cast<int>(ldec);
+  d->Nr = p->window;
+  d->Natt = p->n_att;
+  d->mode = p->mode;
+  const bool diag = p->mode == DSA_MODE_DIAGONAL;
+  d->plan_cap = diag ? static_cast<int>(std::min<int64_t>(p->n_att, ldec)) : 0;
+  d->state_cap = p->window - p->n_att;
+  if (pairs * std::max(d->plan_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
+  if (pairs * std::max(d->state_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
+
+  // plan buffer: count | flags | indices
+  size_t off = 0;
+  d->plan.count_offset = off;
+  off = align_up(off + 4 * pairs, 256);
+  d->plan.flags_offset = off;
+  off = align_up(off + 4 * pairs, 256);
+  d->plan.indices_offset = off;
+  off = align_up(off + 4 * static_cast<size_t>(pairs) * d->plan_cap, 256);
+  d->plan.cap = d->plan_cap;
+  d->plan.bytes = off;
+
+  // state buffer: count | flags | offsets (uint16)
+  off = 0;
+  d->state.count_offset = off;
+  off = align_up(off + 4 * pairs, 256);
+  d->state.flags_offset = off;
+  off = align_up(off + 4 * pairs, 256);
+  d->state.offsets_offset = off;
+  off = align_up(off + 2 * static_cast<size_t>(pairs) * d->state_cap, 256);
+  d->state.cap = d->state_cap;
+  d->state.bytes = off;
+
+  // Split configuration of the decode kernel.  A wave loads rows_per_instr
+  // rows per 16-byte-per-lane load, U loads deep; a split holds C rows (a
+  // multiple of that block) and aims at ~48 KB of K+V so that every request
+  // is cut into a few workgroups and the grid has enough waves in flight.
+  const int rows_per_instr = 512 / d->D;  // 8 for d=64, 4 for d=128
+  d->U = env_int("DSA_TUNE_UNROLL", 2) >= 4 ? 4 : 2;
+  const int block_rows = rows_per_instr * d->U;
+  const int64_t rows_max = d->Lp + (diag ? d->plan_cap : ldec);
+  d->rows_max = static_cast<int>(rows_max);
+  const int64_t split_bytes = env_int("DSA_TUNE_SPLIT_KB", 48) * int64_t(1024);
+  const int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
+  int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
+  const int64_t min_wgs = env_int("DSA_TUNE_MIN_WGS", 512);
+  if (pairs * S < min_wgs) {
+    const int64_t want = (min_wgs + pairs - 1) / pairs;
+    const int64_t most = std::max<int64_t>(1, (rows_max + block_rows - 1) / block_rows);
+    S = std::max<int64_t>(S, std::min(want, most));
+  }
+  int64_t C = (rows_max + S - 1) / S;
+  C = std::max<int64_t>(block_rows, (C + block_rows - 1) / block_rows * block_rows);
+  S = std::max<int64_t>(1, (rows_max + C - 1) / C);
+  if (pairs * S > (int64_t(1) << 31) - 1) return DSA_ERR_INVALID_ARG;
+  d->C = static_cast<int>(C);
+  d->S = static_cast<int>(S);
+  d->ws_bytes = S > 1 ? static_cast<size_t>(pairs) * S * G * (d->D + 2) * sizeof(float) : 0;
+  return DSA_OK;
+}
+
+}  // namespace dsa
+
+using dsa::Derived;
+
+extern "C" {
+
+DSA_API int32_t dsa_abi_version(void) { return DSA_ABI_VERSION; }
+
+DSA_API const char* dsa_status_str(dsa_status st) {
+  switch (st) {
+    case DSA_OK: return "ok";
+    case DSA_ERR_INVALID_ARG: return "invalid argument";
+    case DSA_ERR_UNSUPPORTED: return "unsupported head_dim or head group size";
+    case DSA_ERR_WORKSPACE: return "caller buffer too small";
+    case DSA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+DSA_API dsa_status dsa_params_from_sparsity(int32_t prompt_len, int32_t grid_h, int32_t grid_w,
+                                            int32_t window, int32_t sparsity_permille,
+                                            int32_t mode, dsa_params* out) {
+  if (!out || sparsity_permille < 0 || sparsity_permille > 1000) return DSA_ERR_INVALID_ARG;
+  if (prompt_len < 0 || grid_h < 1 || grid_w < 1 || window < 0 || window > 65535)
+    return DSA_ERR_INVALID_ARG;
+  if (mode != DSA_MODE_DENSE && mode != DSA_MODE_DIAGONAL) return DSA_ERR_INVALID_ARG;
+  const int64_t ldec = static_cast<int64_t>(grid_h) * grid_w;
+  if (ldec > (1 << 24)) return DSA_ERR_INVALID_ARG;
+  int64_t nr = window;
+  if (nr == 0) nr = std::max<int64_t>(1, std::min<int64_t>(ldec / 2, 65535));
+  // round((1 - s) * L_dec) with ties up: floor((2 * (1000 - s) * L_dec + 1000) / 2000)
+  int64_t natt = (2 * (1000 - int64_t(sparsity_permille)) * ldec + 1000) / 2000;
+  natt = std::min(nr, std::max<int64_t>(1, natt));
+  out->prompt_len = prompt_len;
+  out->grid_h = grid_h;
+  out->grid_w = grid_w;
+  out->window = static_cast<int32_t>(nr);
+  out->n_att = static_cast<int32_t>(natt);
+  out->mode = mode;
+  return DSA_OK;
+}
+
+DSA_API dsa_status dsa_validate(const dsa_params* p, const dsa_shape* s) {
+  Derived d;
+  return dsa::derive(p, s, &d);
+}
+
+DSA_API dsa_status dsa_get_state_layout(const dsa_params* p, const dsa_shape* s,
+                                        dsa_state_layout* out) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!out) return DSA_ERR_INVALID_ARG;
+  *out = d.state;
+  return DSA_OK;
+}
+
+DSA_API dsa_status dsa_get_plan_layout(const dsa_params* p, const dsa_shape* s,
+                                       dsa_plan_layout* out) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!out) return DSA_ERR_INVALID_ARG;
+  *out = d.plan;
+  return DSA_OK;
+}
+
+DSA_API dsa_status dsa_get_launch_info(const dsa_params* p, const dsa_shape* s,
+                                       dsa_launch_info* out) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!out) return DSA_ERR_INVALID_ARG;
+  out->rows_per_split = d.C;
+  out->max_splits = d.S;
+  out->workgroups = d.B * d.Hkv * d.S;
+  out->kernel_variant = d.U;
+  out->workspace_bytes = d.ws_bytes;
+  return DSA_OK;
+}
+
+DSA_API size_t dsa_state_bytes(const dsa_params* p, const dsa_shape* s) {
+  Derived d;
+  return dsa::derive(p, s, &d) == DSA_OK ? d.state.bytes : 0;
+}
+
+DSA_API size_t dsa_plan_bytes(const dsa_params* p, const dsa_shape* s) {
+  Derived d;
+  return dsa::derive(p, s, &d) == DSA_OK ? d.plan.bytes : 0;
+}
+
+DSA_API size_t dsa_workspace_bytes(const dsa_params* p, const dsa_shape* s) {
+  Derived d;
+  return dsa::derive(p, s, &d) == DSA_OK ? d.ws_bytes : 0;
+}
+
+DSA_API size_t dsa_window_logits_count(const dsa_params* p, const dsa_shape* s) {
+  Derived d;
+  return dsa::derive(p, s, &d) == DSA_OK
+             ? static_cast<size_t>(d.B) * d.Hq * d.plan_cap
+             : 0;
+}
+
+static dsa_status hip_status(hipError_t launch) {
+  if (launch != hipSuccess) return DSA_ERR_HIP;
+  return hipGetLastError() == hipSuccess ? DSA_OK : DSA_ERR_HIP;
+}
+
+DSA_API dsa_status dsa_state_reset(const dsa_params* p, const dsa_shape* s, void* d_state,
+                                   const int32_t* d_req_mask, hipStream_t stream) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!d_state) return DSA_ERR_INVALID_ARG;
+  char* base = static_cast<char*>(d_state);
+  dsa::ResetArgs a{};
+  a.st_count = reinterpret_cast<int32_t*>(base + d.state.count_offset);
+  a.st_flags = reinterpret_cast<int32_t*>(base + d.state.flags_offset);
+  a.mask = d_req_mask;
+  a.pairs = d.B * d.Hkv;
+  a.Hkv = d.Hkv;
+  return hip_status(dsa::launch_reset(d, a, stream));
+}
+
+DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,
+                            const void* d_state, void* d_plan, size_t plan_bytes,
+                            hipStream_t stream) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!d_decode_pos || !d_plan) return DSA_ERR_INVALID_ARG;
+  if (d.mode == DSA_MODE_DIAGONAL && !d_state) return DSA_ERR_INVALID_ARG;
+  if (plan_bytes < d.plan.bytes) return DSA_ERR_WORKSPACE;
+  char* pb = static_cast<char*>(d_plan);
+  const char* sb = static_cast<const char*>(d_state);
+  dsa::PlanArgs a{};
+  a.pos = d_decode_pos;
+  a.st_count = sb ? reinterpret_cast<const int32_t*>(sb + d.state.count_offset) : nullptr;
+  a.st_off = sb ? reinterpret_cast<const uint16_t*>(sb + d.state.offsets_offset) : nullptr;
+  a.count = reinterpret_cast<int32_t*>(pb + d.plan.count_offset);
+  a.flags = reinterpret_cast<int32_t*>(pb + d.plan.flags_offset);
+  a.idx = reinterpret_cast<int32_t*>(pb + d.plan.indices_offset);
+  a.pairs = d.B * d.Hkv;
+  a.Hkv = d.Hkv;
+  a.Ldec = d.Ldec;
+  a.Nr = d.Nr;
+  a.Natt = d.Natt;
+  a.mode = d.mode;
+  a.plan_cap = d.plan_cap;
+  a.state_cap = d.state_cap;
+  a.words = (d.Nr + 31) / 32;
+  return hip_status(dsa::launch_plan(d, a, stream));
+}
+
+DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                        const void* d_k, const void* d_v,
+                                        const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                        const void* d_plan, float sm_scale, float* d_out,
+                                        float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                        hipStream_t stream) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (!d_q || !d_k || !d_v || !kv || !d_decode_pos || !d_out) return DSA_ERR_INVALID_ARG;
+  if (d.mode == DSA_MODE_DIAGONAL && !d_plan) return DSA_ERR_INVALID_ARG;
+  if (!std::isfinite(sm_scale)) return DSA_ERR_INVALID_ARG;
+  if (kv->stride_row < d.D || kv->stride_head < 0 || kv->stride_batch < 0)
+    return DSA_ERR_INVALID_ARG;
+  if ((kv->stride_row | kv->stride_head | kv->stride_batch) & 7) return DSA_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(d_k) | reinterpret_cast<uintptr_t>(d_v) |
+       reinterpret_cast<uintptr_t>(d_q)) & 15)
+    return DSA_ERR_INVALID_ARG;
+  if (d.ws_bytes && (!d_ws || ws_bytes < d.ws_bytes)) return DSA_ERR_WORKSPACE;
+  const char* pb = static_cast<const char*>(d_plan);
+  dsa::DecodeArgs a{};
+  a.q = static_cast<const uint16_t*>(d_q);
+  a.k = static_cast<const uint16_t*>(d_k);
+  a.v = static_cast<const uint16_t*>(d_v);
+  a.row_base = kv->d_row_base;
+  a.sb = kv->stride_batch;
+  a.sh = kv->stride_head;
+  a.sr = kv->stride_row;
+  a.pos = d_decode_pos;
+  a.count = pb ? reinterpret_cast<const int32_t*>(pb + d.plan.count_offset) : nullptr;
+  a.idx = pb ? reinterpret_cast<const int32_t*>(pb + d.plan.indices_offset) : nullptr;
+  a.scale = sm_scale;
+  a.scale_log2 = sm_scale * 1.4426950408889634f;
+  a.out = d_out;
+  a.wlog = d.mode == DSA_MODE_DIAGONAL ? d_window_logits : nullptr;
+  a.part = static_cast<float*>(d_ws);
+  a.B = d.B;
+  a.Hq = d.Hq;
+  a.Hkv = d.Hkv;
+  a.Lp = d.Lp;
+  a.Ldec = d.Ldec;
+  a.mode = d.mode;
+  a.plan_cap = d.plan_cap;
+  a.C = d.C;
+  a.S = d.S;
+  return hip_status(dsa::launch_decode(d, a, stream));
+}
+
+DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,
+                              const void* d_plan, const float* d_window_logits, void* d_state,
+                              hipStream_t stream) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (d.mode != DSA_MODE_DIAGONAL) return DSA_OK;  // dense mode keeps no selection
+  if (!d_decode_pos || !d_plan || !d_window_logits || !d_state) return DSA_ERR_INVALID_ARG;
+  if (d.state_cap == 0) return DSA_OK;  // N_att == N_r: nothing is ever skipped
+  const char* pb = static_cast<const char*>(d_plan);
+  char* sb = static_cast<char*>(d_state);
+  dsa::SelectArgs a{};
+  a.pos = d_decode_pos;
+  a.count = reinterpret_cast<const int32_t*>(pb + d.plan.count_offset);
+  a.idx = reinterpret_cast<const int32_t*>(pb + d.plan.indices_offset);
+  a.wlog = d_window_logits;
+  a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
+  a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
+  a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+  a.pairs = d.B * d.Hkv;
+  a.Hq = d.Hq;
+  a.Hkv = d.Hkv;
+  a.G = d.G;
+  a.Ldec = d.Ldec;
+  a.Nr = d.Nr;
+  a.Natt = d.Natt;
+  a.plan_cap = d.plan_cap;
+  a.state_cap = d.state_cap;
+  return hip_status(dsa::launch_select(d, a, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,85 @@
+// Internal declarations shared by the library's translation units: the
+// derived launch configuration, the kernel argument blocks and the launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "dsa.h"
+
+namespace dsa {
+
+// Everything a call needs, derived once from (params, shape) on the host.
+struct Derived {
+  int B, Hq, Hkv, G, D;
+  int Lp, Ldec, Nr, Natt, mode;
+  int plan_cap;   // kept decode rows per (request, KV head): min(N_att, L_dec), 0 when dense
+  int state_cap;  // skip entries per (request, KV head): N_r - N_att
+  dsa_plan_layout plan;
+  dsa_state_layout state;
+  int rows_max;   // prompt rows + the most decode rows one request can attend
+  int U;          // loads in flight per wave per operand (unroll)
+  int C;          // rows per split workgroup
+  int S;          // splits per (request, KV head), upper bound
+  size_t ws_bytes;
+};
+
+dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
+
+constexpr int kWaves = 4;          // waves per workgroup in every kernel
+constexpr int kBlock = 64 * kWaves;
+constexpr float kNegBig = -1.0e30f;  // "no score yet": finite, so exp2 of a difference is 0
+
+struct PlanArgs {
+  const int32_t* pos;
+  const int32_t* st_count;
+  const uint16_t* st_off;
+  int32_t* count;
+  int32_t* flags;
+  int32_t* idx;
+  int pairs, Hkv, Ldec, Nr, Natt, mode, plan_cap, state_cap, words;
+};
+
+struct DecodeArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  const int64_t* row_base;
+  int64_t sb, sh, sr;
+  const int32_t* pos;
+  const int32_t* count;  // plan counts (diagonal mode)
+  const int32_t* idx;    // plan indices (diagonal mode)
+  float scale;           // sm_scale
+  float scale_log2;      // sm_scale * log2(e)
+  float* out;
+  float* wlog;           // window logits or nullptr
+  float* part;           // split partials (S > 1)
+  int B, Hq, Hkv, Lp, Ldec, mode, plan_cap, C, S;
+};
+
+struct SelectArgs {
+  const int32_t* pos;
+  const int32_t* count;  // plan counts
+  const int32_t* idx;    // plan indices
+  const float* wlog;
+  int32_t* st_count;
+  int32_t* st_flags;
+  uint16_t* st_off;
+  int pairs, Hq, Hkv, G, Ldec, Nr, Natt, plan_cap, state_cap;
+};
+
+struct ResetArgs {
+  int32_t* st_count;
+  int32_t* st_flags;
+  const int32_t* mask;
+  int pairs, Hkv;
+};
+
+hipError_t launch_plan(const Derived& d, const PlanArgs& a, hipStream_t st);
+hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st);
+hipError_t launch_select(const Derived& d, const SelectArgs& a, hipStream_t st);
+hipError_t launch_reset(const Derived& d, const ResetArgs& a, hipStream_t st);
+
+}  // namespace dsa

@@ -1,0 +1,121 @@
+"""Drive the library over a synthetic multi-layer decode batch.
+
+``Layer`` holds one layer's device tensors (KV cache, queries, selection
+state, plan, logits, workspace, output).  ``build_histories`` gives every
+(request, KV head) the skip list Algorithm 1 would have built before its
+current decode position, by running the library's own plan -> decode ->
+select pipeline over the phase-2 steps with per-step synthetic queries:
+at step ``u`` a request whose position ``t_b`` is still ahead runs at
+position ``u``, and the others are marked unused (position -1).
+
+``step`` runs one decode step (all layers) in diagonal or dense mode; every
+launch goes to the current torch stream and nothing synchronises.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+from typing import List, Optional
+
+import torch
+
+from . import binding as B
+from . import synth
+
+
+@dataclass
+class Layer:
+    kv: synth.LayerKV
+    q: torch.Tensor
+    bufs: B.Buffers
+
+
+@dataclass
+class Batch:
+    w: synth.Workload
+    p: B.Params          # diagonal-mode parameters
+    pd: B.Params         # the same with dense mode
+    s: B.Shape
+    pos: torch.Tensor    # int32 [B] on the device
+    pos_host: List[int]
+    layers: List[Layer]
+    dense_bufs: B.Buffers
+    scale: float
+
+    def kv_bytes(self, dense: bool) -> int:
+        """Algorithmic K+V bytes one step streams over all layers: 4*d bytes
+        (a bf16 K row and V row) per attended key per KV head."""
+        n_att = self.p.n_att
+        rows = 0
+        for t in self.pos_host:
+            if t < 0:
+                continue
+            rows += self.w.prompt_len + (t + 1 if dense else min(t + 1, n_att))
+        return rows * self.s.num_kv_heads * 4 * self.s.head_dim * len(self.layers)
+
+
+def make_batch(w: synth.Workload, layers: Optional[int] = None, device="cuda",
+               positions: Optional[List[int]] = None) -> Batch:
+    nl = w.layers if layers is None else layers
+    p = B.params_from_sparsity(w.prompt_len, w.grid_h, w.grid_w, w.window, w.sparsity_permille,
+                               B.MODE_DIAGONAL)
+    pd = B.make_params(p.prompt_len, p.grid_h, p.grid_w, p.window, p.n_att, B.MODE_DENSE)
+    s = B.make_shape(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim)
+    pos_host = list(positions) if positions is not None else synth.positions(w).tolist()
+    pos = torch.tensor(pos_host, dtype=torch.int32, device=device)
+    rows = max(max(pos_host) + 1, 1)
+    out = []
+    for layer in range(nl):
+        kv = synth.layer_kv(w, layer, device, decode_rows=rows)
+        q = synth.layer_query(w, layer, device)
+        out.append(Layer(kv, q, B.alloc_buffers(p, s, device)))
+    dense_bufs = B.alloc_buffers(pd, s, device)
+    return Batch(w, p, pd, s, pos, pos_host, out, dense_bufs, 1.0 / math.sqrt(w.head_dim))
+
+
+def build_histories(bt: Batch, device="cuda"):
+    """Run the phase-2 steps of every layer so that each state holds the skip
+    entries appended before its request's decode position."""
+    p, s, w = bt.p, bt.s, bt.w
+    last = min(max(bt.pos_host) - 1, p.window - 2)
+    for li, L in enumerate(bt.layers):
+        B.state_reset(p, s, L.bufs.state)
+        for u in range(p.n_att - 1, last + 1):
+            pos = torch.tensor([u if u < t else -1 for t in bt.pos_host], dtype=torch.int32,
+                               device=device)
+            q = synth.step_query(w, li, u, device)
+            B.plan(p, s, pos, L.bufs.state, L.bufs.plan)
+            B.decode_attention(p, s, q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), pos, L.bufs.plan,
+                               bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace)
+            B.select(p, s, pos, L.bufs.plan, L.bufs.logits, L.bufs.state)
+
+
+def sparse_layer(bt: Batch, L: Layer, timer=None):
+    p, s = bt.p, bt.s
+    B.plan(p, s, bt.pos, L.bufs.state, L.bufs.plan)
+    if timer is not None:
+        timer[0].record()
+    B.decode_attention(p, s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, L.bufs.plan,
+                       bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace)
+    if timer is not None:
+        timer[1].record()
+    B.select(p, s, bt.pos, L.bufs.plan, L.bufs.logits, L.bufs.state)
+
+
+def dense_layer(bt: Batch, L: Layer, timer=None):
+    db = bt.dense_bufs
+    if timer is not None:
+        timer[0].record()
+    B.decode_attention(bt.pd, bt.s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, None,
+                       bt.scale, db.out, None, db.workspace)
+    if timer is not None:
+        timer[1].record()
+
+
+def step(bt: Batch, dense: bool = False, timers=None):
+    """One decode step over all layers; ``timers[i]`` (a pair of events) is
+    recorded around layer i's attention launch when given."""
+    fn = dense_layer if dense else sparse_layer
+    for i, L in enumerate(bt.layers):
+        fn(bt, L, None if timers is None else timers[i])

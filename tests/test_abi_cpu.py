@@ -1,0 +1,110 @@
+"""Host-side checks of libdsa.so that need no GPU: the library loads, exports
+every entry point ``include/dsa.h`` declares, and its host logic (parameter
+rule, validation, buffer layouts, split configuration) is right.  No device
+work is launched here."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import params as oparams
+from paper_2609_19702_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "dsa.h")).read()
+    return sorted(set(re.findall(r"DSA_API\s+[\w\s\*]+?\b(dsa_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_symbols()
+    assert len(names) >= 15
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(B.SIGNATURES), "binding and header disagree"
+    assert B.abi_version() == 1
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4):
+        assert B.status_str(st) and "unknown" not in B.status_str(st)
+    assert "unknown" in B.status_str(7)
+
+
+@pytest.mark.parametrize("h,w,window,permille", [
+    (24, 24, 128, 950), (24, 24, 256, 900), (64, 64, 512, 950), (16, 16, 64, 950),
+    (16, 16, 64, 900), (96, 96, 64, 950), (2, 2, 4, 875), (4, 4, 8, 0), (3, 5, 15, 1000),
+    (48, 48, 1024, 950), (7, 11, 33, 333),
+])
+def test_params_from_sparsity_matches_oracle(h, w, window, permille):
+    p = B.params_from_sparsity(10, h, w, window, permille)
+    assert p.n_att == oparams.n_att_from_sparsity(h, w, window, permille)
+    assert p.window == window
+
+
+def test_default_window():
+    p = B.params_from_sparsity(0, 24, 24, 0, 950)
+    assert p.window == oparams.default_window(24, 24)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(prompt_len=-1), dict(grid_h=0), dict(window=0), dict(window=70000), dict(n_att=0),
+    dict(n_att=200), dict(mode=2),
+])
+def test_validate_rejects_bad_params(bad):
+    kw = dict(prompt_len=8, grid_h=8, grid_w=8, window=32, n_att=8, mode=1)
+    kw.update(bad)
+    p = B.make_params(**kw)
+    assert B.validate(p, B.make_shape(2, 4, 4, 64)) == B.ERR_INVALID_ARG
+    assert B.plan_bytes(p, B.make_shape(2, 4, 4, 64)) == 0
+
+
+def test_validate_shapes():
+    p = B.make_params(8, 8, 8, 32, 8)
+    assert B.validate(p, B.make_shape(2, 4, 4, 64)) == B.OK
+    assert B.validate(p, B.make_shape(2, 32, 8, 128)) == B.OK
+    assert B.validate(p, B.make_shape(2, 6, 4, 64)) == B.ERR_INVALID_ARG   # 6 % 4
+    assert B.validate(p, B.make_shape(0, 4, 4, 64)) == B.ERR_INVALID_ARG
+    assert B.validate(p, B.make_shape(2, 4, 4, 96)) == B.ERR_UNSUPPORTED
+    assert B.validate(p, B.make_shape(2, 12, 4, 64)) == B.ERR_UNSUPPORTED  # group 3
+
+
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("shape,par", [
+    ((64, 20, 20, 64), (120, 24, 24, 128, 950)),
+    ((128, 32, 32, 128), (256, 24, 24, 256, 950)),
+    ((32, 32, 8, 128), (256, 64, 64, 512, 950)),
+    ((1, 8, 8, 64), (32, 16, 16, 64, 950)),
+    ((256, 32, 32, 128), (256, 96, 96, 1024, 950)),
+    ((3, 8, 1, 64), (0, 5, 7, 9, 500)),
+])
+def test_layouts_and_split_config(mode, shape, par):
+    p = B.params_from_sparsity(*par, mode=mode)
+    s = B.make_shape(*shape)
+    pairs = s.batch * s.num_kv_heads
+    pl, sl, li = B.plan_layout(p, s), B.state_layout(p, s), B.launch_info(p, s)
+    L_dec = p.grid_h * p.grid_w
+    assert pl.cap == (min(p.n_att, L_dec) if mode == 1 else 0)
+    assert sl.cap == p.window - p.n_att
+    for off in (pl.count_offset, pl.flags_offset, pl.indices_offset,
+                sl.count_offset, sl.flags_offset, sl.offsets_offset):
+        assert off % 256 == 0
+    assert pl.flags_offset >= pl.count_offset + 4 * pairs
+    assert pl.indices_offset >= pl.flags_offset + 4 * pairs
+    assert pl.bytes == B.plan_bytes(p, s) and pl.bytes >= pl.indices_offset + 4 * pairs * pl.cap
+    assert sl.bytes == B.state_bytes(p, s) and sl.bytes >= sl.offsets_offset + 2 * pairs * sl.cap
+    rows_max = p.prompt_len + (pl.cap if mode == 1 else L_dec)
+    block = (512 // s.head_dim) * li.kernel_variant
+    assert li.rows_per_split % block == 0
+    assert li.rows_per_split * li.max_splits >= rows_max
+    assert li.rows_per_split * (li.max_splits - 1) < max(rows_max, 1)
+    assert li.workgroups == pairs * li.max_splits
+    g = s.num_q_heads // s.num_kv_heads
+    want_ws = pairs * li.max_splits * g * (s.head_dim + 2) * 4 if li.max_splits > 1 else 0
+    assert li.workspace_bytes == want_ws == B.workspace_bytes(p, s)
+    assert B.window_logits_count(p, s) == s.batch * s.num_q_heads * pl.cap
