@@ -4,15 +4,19 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
 One step is one decode step of the whole hot path over every layer of the
-workload: ``dsa_plan -> dsa_decode_attention (split-K + combine) ->
-dsa_select`` per layer, all inputs resident in HBM.  The dense mode of the
+workload, all inputs resident in HBM: per layer the fused ``dsa_decode_step``
+(kept-set construction, split-K attention, combine and phase-2 selection in
+one pass; ``value``), and for comparison the same work as three calls
+``dsa_plan -> dsa_decode_attention -> dsa_select`` (``separate_calls``).  The step is captured
+once as a HIP graph and replayed (``--eager`` launches it from Python
+instead).  The dense mode of the
 same kernels, on the same inputs and positions, is timed alongside for the
 speedup.  Prints one JSON line.
 
 ``roofline`` describes the decode kernel (the dominant one): algorithmic K/V
 bytes per launch (4*d bytes per attended key per KV head) divided by its
-mean launch time from HIP events recorded around every launch inside the
-timed steps.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
+mean launch time, from HIP events that the extended launch binds to the
+kernel's own start and end, over ``--steps`` further eager steps.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
 of the same workload (``--no-cpu-baseline`` skips it).
 """
 
@@ -42,6 +46,7 @@ def parse():
     ap.add_argument("--workload", default="llamagen_xl")
     ap.add_argument("--positions", default=None, help="ragged | last | first")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     return ap.parse_args()
 
@@ -113,22 +118,48 @@ def cpu_baseline(bt, seconds):
                        f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
 
 
-def timed(bt, steps, dense):
+def capture(bt, mode):
+    """The whole decode step (every layer) as one HIP graph."""
     import torch
     from paper_2609_19702_amd import workload
-    n = len(bt.layers)
-    timers = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(n)] for _ in range(steps)]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run_step(bt, mode)
+    return g
+
+
+def run_step(bt, mode, timers=None):
+    from paper_2609_19702_amd import workload
+    workload.step(bt, dense=mode == "dense", fused=mode == "fused", timers=timers)
+
+
+def timed_steps(bt, steps, mode, graph):
+    """ms per step over ``steps`` steps (graph replays, or eager launches)."""
+    import torch
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
-    for k in range(steps):
-        workload.step(bt, dense=dense, timers=timers[k])
+    for _ in range(steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            run_step(bt, mode)
     end.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / steps
-    launch = [a.elapsed_time(b) for row in timers for (a, b) in row]
-    return ms, launch
+    return start.elapsed_time(end) / steps
+
+
+def kernel_times(bt, steps, mode):
+    """Per-launch duration (ms) of the split-K decode kernel over ``steps``
+    eager steps, from events bound to the kernel's own start and end."""
+    import torch
+    from paper_2609_19702_amd import binding as B
+    timers = [[B.timing_events() for _ in bt.layers] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for k in range(steps):
+        run_step(bt, mode, timers=timers[k])
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for row in timers for (a, b) in row]
 
 
 def main():
@@ -154,13 +185,24 @@ def main():
     print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
           f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
 
+    modes = ("fused", "separate", "dense")
     for _ in range(args.warmup):
-        workload.step(bt, dense=False)
-        workload.step(bt, dense=True)
+        for mode in modes:
+            run_step(bt, mode)
     torch.cuda.synchronize()
-    ms_sparse, launch_sparse = timed(bt, args.steps, dense=False)
-    ms_dense, launch_dense = timed(bt, args.steps, dense=True)
-    print(f"# sparse {ms_sparse:.3f} ms/step, dense {ms_dense:.3f} ms/step", file=sys.stderr, flush=True)
+    graphs = {m: (None if args.eager else capture(bt, m)) for m in modes}
+    for g in graphs.values():
+        if g is not None:
+            g.replay()
+    torch.cuda.synchronize()
+    ms = {m: timed_steps(bt, args.steps, m, graphs[m]) for m in modes}
+    launch = {m: kernel_times(bt, args.steps, m) for m in modes}
+    ms_sparse, ms_dense = ms["fused"], ms["dense"]
+    launch_sparse, launch_dense = launch["fused"], launch["dense"]
+    print(f"# ms/step ({'eager' if args.eager else 'graph'}): "
+          + ", ".join(f"{m} {ms[m]:.3f}" for m in modes)
+          + "; decode kernel us: " + ", ".join(f"{m} {statistics.fmean(launch[m]) * 1e3:.2f}" for m in modes),
+          file=sys.stderr, flush=True)
 
     n_layers = len(bt.layers)
     bytes_sparse = bt.kv_bytes(dense=False)
@@ -197,6 +239,7 @@ def main():
             "n_att": bt.p.n_att, "sparsity": round(1 - bt.p.n_att / w.decode_len, 4),
             "positions": w.positions, "accumulate": "fp32",
             "splits": info.max_splits, "rows_per_split": info.rows_per_split,
+            "launch": "eager" if args.eager else "hip_graph",
         },
         "kv_gbps": bytes_sparse / (ms_sparse * 1e-3) / 1e9,
         "kv_hbm_frac": bytes_sparse / (ms_sparse * 1e-3) / 1e9 / HBM_PEAK_GBPS,
@@ -206,12 +249,17 @@ def main():
             "decode_launch_us": dense_launch_ms * 1e3,
             "decode_launch_gbps": bytes_dense / n_layers / (dense_launch_ms * 1e-3) / 1e9,
         },
+        "separate_calls": {
+            "ms_per_step": ms["separate"], "tokens_per_s": w.batch / (ms["separate"] * 1e-3),
+            "decode_launch_us": statistics.fmean(launch["separate"]) * 1e3,
+        },
         "speedup_vs_dense": ms_dense / ms_sparse,
         "ideal_speedup": bytes_dense / bytes_sparse,
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-            "kernel": "decode_kernel (+ combine when split)", "bytes_per_launch": per_launch,
+            "kernel": "decode_kernel (fused step)", "bytes_per_launch": per_launch,
+            "launches_timed": len(launch_sparse),
             "launch_us": mean_launch_ms * 1e3, "source_hash": src_hash,
         },
         "cpu_baseline": base,

@@ -261,6 +261,59 @@ DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s,
                                         hipStream_t stream);
 
 /*
+ * dsa_decode_attention with its split-K kernel launched so that the two
+ * events receive that kernel's own start and end timestamps (the AMD
+ * extended launch); hipEventElapsedTime(decode_start, decode_stop) is then
+ * the kernel's execution time, without queueing or launch gaps.  The events
+ * must already exist (hipEventCreate).  For profiling tools; not usable
+ * inside a HIP graph capture.  Errors as dsa_decode_attention, and
+ * INVALID_ARG for a NULL event.
+ */
+DSA_API dsa_status dsa_decode_attention_timed(const dsa_params* p, const dsa_shape* s,
+                                              const void* d_q, const void* d_k, const void* d_v,
+                                              const dsa_kv_layout* kv,
+                                              const int32_t* d_decode_pos, const void* d_plan,
+                                              float sm_scale, float* d_out,
+                                              float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                              hipEvent_t decode_start, hipEvent_t decode_stop,
+                                              hipStream_t stream);
+
+/*
+ * One whole decode step of one layer in a single pass over the KV:
+ * exactly dsa_plan -> dsa_decode_attention -> dsa_select (diagonal mode)
+ * with bit-identical plan, window logits, output and selection state, the
+ * way the paper's own kernel fuses the index gather and the window argmin
+ * into the attention (section 5.1, "Implementation").  Every decode
+ * workgroup rebuilds the kept set of its (request, KV head) from d_state;
+ * when one split covers a (request, KV head) it also runs the phase-2
+ * argmin and appends the skip entry, otherwise a second kernel merges the
+ * splits and selects.  In dense mode it is dsa_decode_attention and d_state,
+ * d_plan and d_window_logits are not used.
+ *   d_state          selection state, in/out (diagonal mode)
+ *   d_plan           plan of this step, out; plan_bytes >= dsa_plan_bytes()
+ *   d_window_logits  fp32 [B][Hq][cap], out; required in diagonal mode
+ *   other arguments  as for dsa_decode_attention
+ * Errors: as dsa_decode_attention; UNSUPPORTED for N_r > 16384 in diagonal
+ * mode (use the three separate calls there).
+ */
+DSA_API dsa_status dsa_decode_step(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                   const void* d_k, const void* d_v, const dsa_kv_layout* kv,
+                                   const int32_t* d_decode_pos, void* d_state, void* d_plan,
+                                   size_t plan_bytes, float sm_scale, float* d_out,
+                                   float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
+/* dsa_decode_step with the split kernel's own start/end timestamps recorded
+ * into two existing events (as dsa_decode_attention_timed). */
+DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                         const void* d_k, const void* d_v,
+                                         const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                         void* d_state, void* d_plan, size_t plan_bytes,
+                                         float sm_scale, float* d_out, float* d_window_logits,
+                                         void* d_ws, size_t ws_bytes, hipEvent_t decode_start,
+                                         hipEvent_t decode_stop, hipStream_t stream);
+
+/*
  * Phase-2 selection of Algorithm 1: for every request with
  * N_att - 1 <= t_b <= N_r - 2 and every KV head h, compute
  *   w_q = softmax(window logits of query head q)   over the kept window

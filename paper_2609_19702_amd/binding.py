@@ -92,6 +92,14 @@ SIGNATURES = {
     "dsa_plan": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.c_size_t, _VP]),
     "dsa_decode_attention": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP, _VP,
                                          C.c_float, _VP, _VP, _VP, C.c_size_t, _VP]),
+    "dsa_decode_attention_timed": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP,
+                                               _VP, C.c_float, _VP, _VP, _VP, C.c_size_t, _VP,
+                                               _VP, _VP]),
+    "dsa_decode_step": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP, _VP, _VP,
+                                    C.c_size_t, C.c_float, _VP, _VP, _VP, C.c_size_t, _VP]),
+    "dsa_decode_step_timed": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP, _VP,
+                                          _VP, C.c_size_t, C.c_float, _VP, _VP, _VP, C.c_size_t,
+                                          _VP, _VP, _VP]),
     "dsa_select": (C.c_int32, [_P, _S, _VP, _VP, _VP, _VP, _VP]),
 }
 
@@ -219,13 +227,42 @@ def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None) -> KVLay
 
 
 def decode_attention(p, s, q, k, v, layout: KVLayout, decode_pos, plan_buf, sm_scale, out,
-                     window_logits=None, workspace=None, stream=None):
+                     window_logits=None, workspace=None, stream=None, events=None):
+    """``events``: optional (start, stop) pair from ``timing_events()``; they
+    then receive the split-K kernel's own start and end timestamps."""
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().dsa_decode_attention(C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v),
-                                      C.byref(layout), _ptr(decode_pos), _ptr(plan_buf),
-                                      float(sm_scale), _ptr(out), _ptr(window_logits),
-                                      _ptr(workspace), ws_bytes, _stream(stream)),
-           "dsa_decode_attention")
+    args = (C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v), C.byref(layout), _ptr(decode_pos),
+            _ptr(plan_buf), float(sm_scale), _ptr(out), _ptr(window_logits), _ptr(workspace),
+            ws_bytes)
+    if events is None:
+        _check(lib().dsa_decode_attention(*args, _stream(stream)), "dsa_decode_attention")
+    else:
+        _check(lib().dsa_decode_attention_timed(*args, events[0].cuda_event, events[1].cuda_event,
+                                                _stream(stream)), "dsa_decode_attention_timed")
+
+
+def decode_step(p, s, q, k, v, layout: KVLayout, decode_pos, state, plan_buf, sm_scale, out,
+                window_logits, workspace=None, stream=None, events=None):
+    """One fused decode step: plan + attention + selection in one pass."""
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    pb = 0 if plan_buf is None else plan_buf.numel() * plan_buf.element_size()
+    args = (C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v), C.byref(layout), _ptr(decode_pos),
+            _ptr(state), _ptr(plan_buf), pb, float(sm_scale), _ptr(out), _ptr(window_logits),
+            _ptr(workspace), ws_bytes)
+    if events is None:
+        _check(lib().dsa_decode_step(*args, _stream(stream)), "dsa_decode_step")
+    else:
+        _check(lib().dsa_decode_step_timed(*args, events[0].cuda_event, events[1].cuda_event,
+                                           _stream(stream)), "dsa_decode_step_timed")
+
+
+def timing_events():
+    """A (start, stop) pair of timing events that exist on the device (torch
+    creates its events lazily, at the first record)."""
+    pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    for e in pair:
+        e.record()
+    return pair
 
 
 def select(p, s, decode_pos, plan_buf, window_logits, state, stream=None):

@@ -75,17 +75,20 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->state.cap = d->state_cap;
   d->state.bytes = off;
 
-  // Split configuration of the decode kernel.  A wave loads rows_per_instr
-  // rows per 16-byte-per-lane load, U loads deep; a split holds C rows (a
-  // multiple of that block) and aims at ~48 KB of K+V so that every request
-  // is cut into a few workgroups and the grid has enough waves in flight.
+  // Split configuration of the decode kernel.  A wave issues U loads of
+  // 512/d rows each (one tile) before consuming them; a split holds C rows
+  // (a multiple of the tile) and aims at ~48 KB of K+V so every request is
+  // cut into a few workgroups and the grid keeps enough loads in flight.
   const int rows_per_instr = 512 / d->D;  // 8 for d=64, 4 for d=128
-  d->U = env_int("DSA_TUNE_UNROLL", 2) >= 4 ? 4 : 2;
+  const int u_default = G >= 8 ? 2 : (G >= 4 ? 4 : 8);
+  const int u_env = env_int("DSA_TUNE_UNROLL", u_default);
+  d->U = (u_env == 2 || u_env == 4 || u_env == 8) ? u_env : u_default;
   const int block_rows = rows_per_instr * d->U;
   const int64_t rows_max = d->Lp + (diag ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
   const int64_t split_bytes = env_int("DSA_TUNE_SPLIT_KB", 48) * int64_t(1024);
-  const int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
+  int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
+  if (diag) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
   const int64_t min_wgs = env_int("DSA_TUNE_MIN_WGS", 512);
   if (pairs * S < min_wgs) {
@@ -99,6 +102,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   if (pairs * S > (int64_t(1) << 31) - 1) return DSA_ERR_INVALID_ARG;
   d->C = static_cast<int>(C);
   d->S = static_cast<int>(S);
+  d->NW = static_cast<int>(std::min<int64_t>(kWaves, (C + block_rows - 1) / block_rows));
   d->ws_bytes = S > 1 ? static_cast<size_t>(pairs) * S * G * (d->D + 2) * sizeof(float) : 0;
   return DSA_OK;
 }
@@ -257,17 +261,26 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
   return hip_status(dsa::launch_plan(d, a, stream));
 }
 
-DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s, const void* d_q,
-                                        const void* d_k, const void* d_v,
-                                        const dsa_kv_layout* kv, const int32_t* d_decode_pos,
-                                        const void* d_plan, float sm_scale, float* d_out,
-                                        float* d_window_logits, void* d_ws, size_t ws_bytes,
-                                        hipStream_t stream) {
+// Shared by dsa_decode_attention (fused = false: reads the plan) and
+// dsa_decode_step (fused = true: reads and updates the selection state and
+// writes the plan).
+static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                              const void* d_k, const void* d_v, const dsa_kv_layout* kv,
+                              const int32_t* d_decode_pos, const void* d_plan, float sm_scale,
+                              float* d_out, float* d_window_logits, void* d_ws, size_t ws_bytes,
+                              hipEvent_t t0, hipEvent_t t1, hipStream_t stream,
+                              bool fused = false, void* d_state = nullptr,
+                              size_t plan_bytes = 0) {
   Derived d;
   dsa_status st = dsa::derive(p, s, &d);
   if (st != DSA_OK) return st;
   if (!d_q || !d_k || !d_v || !kv || !d_decode_pos || !d_out) return DSA_ERR_INVALID_ARG;
   if (d.mode == DSA_MODE_DIAGONAL && !d_plan) return DSA_ERR_INVALID_ARG;
+  if (fused && d.mode == DSA_MODE_DIAGONAL) {
+    if (!d_state || !d_window_logits) return DSA_ERR_INVALID_ARG;
+    if (plan_bytes < d.plan.bytes) return DSA_ERR_WORKSPACE;
+    if (d.Nr > dsa::kMaxFusedWindow) return DSA_ERR_UNSUPPORTED;
+  }
   if (!std::isfinite(sm_scale)) return DSA_ERR_INVALID_ARG;
   if (kv->stride_row < d.D || kv->stride_head < 0 || kv->stride_batch < 0)
     return DSA_ERR_INVALID_ARG;
@@ -302,7 +315,71 @@ DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s,
   a.plan_cap = d.plan_cap;
   a.C = d.C;
   a.S = d.S;
-  return hip_status(dsa::launch_decode(d, a, stream));
+  a.Nr = d.Nr;
+  a.Natt = d.Natt;
+  a.state_cap = d.state_cap;
+  a.words = (d.Nr + 31) / 32;
+  if (fused && d.mode == DSA_MODE_DIAGONAL) {
+    char* sb = static_cast<char*>(d_state);
+    char* pbw = static_cast<char*>(const_cast<void*>(d_plan));
+    a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
+    a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
+    a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+    a.plan_count = reinterpret_cast<int32_t*>(pbw + d.plan.count_offset);
+    a.plan_flags = reinterpret_cast<int32_t*>(pbw + d.plan.flags_offset);
+    a.plan_idx = reinterpret_cast<int32_t*>(pbw + d.plan.indices_offset);
+    a.count = nullptr;
+    a.idx = nullptr;
+    return hip_status(dsa::launch_step(d, a, stream, t0, t1));
+  }
+  return hip_status(dsa::launch_decode(d, a, stream, t0, t1));
+}
+
+DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                        const void* d_k, const void* d_v,
+                                        const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                        const void* d_plan, float sm_scale, float* d_out,
+                                        float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                        hipStream_t stream) {
+  return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
+                     d_window_logits, d_ws, ws_bytes, nullptr, nullptr, stream);
+}
+
+DSA_API dsa_status dsa_decode_attention_timed(const dsa_params* p, const dsa_shape* s,
+                                              const void* d_q, const void* d_k, const void* d_v,
+                                              const dsa_kv_layout* kv,
+                                              const int32_t* d_decode_pos, const void* d_plan,
+                                              float sm_scale, float* d_out,
+                                              float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                              hipEvent_t decode_start, hipEvent_t decode_stop,
+                                              hipStream_t stream) {
+  if (!decode_start || !decode_stop) return DSA_ERR_INVALID_ARG;
+  return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
+                     d_window_logits, d_ws, ws_bytes, decode_start, decode_stop, stream);
+}
+
+DSA_API dsa_status dsa_decode_step(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                   const void* d_k, const void* d_v, const dsa_kv_layout* kv,
+                                   const int32_t* d_decode_pos, void* d_state, void* d_plan,
+                                   size_t plan_bytes, float sm_scale, float* d_out,
+                                   float* d_window_logits, void* d_ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
+                     d_window_logits, d_ws, ws_bytes, nullptr, nullptr, stream, true, d_state,
+                     plan_bytes);
+}
+
+DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s, const void* d_q,
+                                         const void* d_k, const void* d_v,
+                                         const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                         void* d_state, void* d_plan, size_t plan_bytes,
+                                         float sm_scale, float* d_out, float* d_window_logits,
+                                         void* d_ws, size_t ws_bytes, hipEvent_t decode_start,
+                                         hipEvent_t decode_stop, hipStream_t stream) {
+  if (!decode_start || !decode_stop) return DSA_ERR_INVALID_ARG;
+  return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
+                     d_window_logits, d_ws, ws_bytes, decode_start, decode_stop, stream, true,
+                     d_state, plan_bytes);
 }
 
 DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,

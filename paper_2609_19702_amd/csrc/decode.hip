@@ -1,10 +1,12 @@
 // Split-K single-query decode attention over the prompt KV plus the kept (or,
-// in dense mode, all) decode KV, and the cross-split log-sum-exp combine.
+// in dense mode, all) decode KV; the cross-split log-sum-exp combine; and the
+// fused decode step that also builds the kept set and runs the phase-2
+// selection.
 //
 // Attn(Q_t, K_p + K[idx], V_p + V[idx]) of Algorithm 1 (section 4) for one
 // (request, KV head, split) per workgroup.  The keys of a (request, KV head)
 // are numbered r = 0 .. n-1: the L_p prompt rows, then the kept decode rows in
-// plan order (dense mode: decode rows 0 .. t).  Split s covers keys
+// ascending position (dense mode: decode rows 0 .. t).  Split s covers keys
 // [s*C, min(n, (s+1)*C)).
 //
 // Data path (HBM-bound: each bf16 K/V element is read once and used for one
@@ -12,49 +14,175 @@
 //   - a lane loads 16 bytes (8 bf16) of a row, so a 64-lane wave loads
 //     512/d rows per instruction with 128-bit coalesced accesses (one row =
 //     d/8 consecutive lanes = one contiguous 128/256-byte segment);
-//   - each wave keeps U row blocks of K and V in flight before using them;
+//   - a wave works on tiles of U load instructions (U*512/d rows) and issues
+//     every K and V load of a tile before using any of them; rows past the
+//     end of the split read a valid row and get weight 0, so no load sits
+//     behind a branch;
+//   - a workgroup has as many waves (1..4) as its split has tiles, so no wave
+//     sits idle holding registers;
+//   - the kept positions of a tile are held one per lane and handed to the
+//     row groups with ds_bpermute; tiles made only of prompt rows need none;
 //   - q.k partial sums are reduced inside the row's lane group with DPP row
 //     permutations (no LDS);
 //   - softmax runs online in fp32 (base-2 exponent with the scale folded
 //     in), one running (max, sum, acc[8]) per lane and query head;
-//   - lane groups, then the 4 waves (through LDS), are merged by log-sum-exp
-//     at the end; one split writes the final output directly, several splits
-//     write fp32 partials (acc[d], max, sum) that the combine kernel merges.
+//   - lane groups, then the waves (through LDS), are merged by log-sum-exp at
+//     the end; one split writes the final output directly, several splits
+//     write fp32 partials (acc[d], max, sum) that a second kernel merges.
+//
+// The fused step (FUSED = true, diagonal mode) reads the selection state
+// instead of a plan: each wave that owns kept decode rows rebuilds the skip
+// set of its (request, KV head) as a bitmap in its own LDS slice and ranks the
+// window positions with ballots, writing the plan as a by-product; when one
+// split covers the whole (request, KV head) the same workgroup then runs the
+// phase-2 argmin on the window logits it computed and appends the skip entry.
+// Every value it produces is bit-identical to dsa_plan -> dsa_decode_attention
+// -> dsa_select.
+#include <hip/hip_ext.h>
+
 #include "device.h"
 #include "internal.h"
 
 namespace dsa {
 namespace {
 
+constexpr int kPre = 8;  // stored skip offsets per lane loaded up front
+
+// Keys of the (request, KV head) and the clamped decode position.
 struct RowRange {
-  int n;     // keys of this (request, KV head); 0 for an unused slot
-  int t;     // decode position after clamping (or -1)
+  int n;      // keys; 0 for an unused slot
+  int t;      // decode position after clamping, or -1
+  int flags;  // DSA_FLAG_INACTIVE / DSA_FLAG_POS_CLAMPED
 };
 
+template <bool FUSED>
 __device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pair) {
-  RowRange r;
+  RowRange r{0, -1, 0};
   int t = a.pos[b];
   if (t < 0) {
-    r.n = 0;
-    r.t = -1;
+    r.flags = DSA_FLAG_INACTIVE;
     return r;
   }
-  t = min(t, a.Ldec - 1);
-  const int nwin = a.mode == DSA_MODE_DENSE ? t + 1 : min(max(a.count[pair], 0), a.plan_cap);
+  if (t >= a.Ldec) {
+    t = a.Ldec - 1;
+    r.flags = DSA_FLAG_POS_CLAMPED;
+  }
+  int nwin;
+  if (a.mode == DSA_MODE_DENSE)
+    nwin = t + 1;
+  else if (FUSED)
+    nwin = min(t + 1, a.Natt);  // the kept count of Algorithm 1 at step t
+  else
+    nwin = min(max(a.count[pair], 0), a.plan_cap);
   r.n = a.Lp + nwin;
   r.t = t;
   return r;
 }
 
-template <int D, int G, int U>
+// Wave-private skip set of one (request, KV head) for the fused step: the
+// bitmap of the first nuse stored offsets, plus the ranking cursor.
+struct SkipSet {
+  uint32_t* bm;
+  int t, dmax;
+  int p0, rank;  // next candidate chunk and kept positions before it
+  int flags;
+};
+
+__device__ __forceinline__ void fence_wave() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, uint32_t* bm,
+                               SkipSet& ss) {
+  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
+  const int cnt = a.st_count[pair];
+  int dv[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int e = lane + 64 * i;
+    dv[i] = e < a.state_cap ? off[e] : 0;
+  }
+  for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
+  const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
+  int flags = cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
+  const int nuse = min(max(cnt, 0), nvalid);
+  fence_wave();
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int e = lane + 64 * i;
+    if (e < nuse) {
+      const int d = dv[i];
+      if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
+    }
+  }
+  for (int e = lane + 64 * kPre; e < nuse; e += 64) {
+    const int d = off[e];
+    if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
+  }
+  if (__ballot(bad)) flags |= DSA_FLAG_BAD_OFFSET;
+  fence_wave();
+  ss.bm = bm;
+  ss.t = t;
+  ss.dmax = min(t, a.Nr - 1);
+  ss.p0 = t - ss.dmax;
+  ss.rank = 0;
+  ss.flags = flags;
+}
+
+__device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
+  if (p > ss.t) return false;
+  const int d = ss.t - p;
+  return ((ss.bm[d >> 5] >> (d & 31)) & 1u) == 0u;
+}
+
+// Kept window positions of ranks [lo, hi) (ascending position), written to
+// kp[rank - kp_base] and to the plan.  The cursor only moves forward, so the
+// tiles of a wave (in increasing rank order) share one scan.
+__device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss, int lo, int hi,
+                            int* kp, int kp_base) {
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
+  while (ss.p0 <= ss.t && ss.rank < hi) {
+    const int p = ss.p0 + lane;
+    const bool kept = is_kept(ss, p);
+    const uint64_t mask = __ballot(kept);
+    const int rk = ss.rank + __popcll(mask & below);
+    if (kept && rk >= lo && rk < hi) {
+      kp[rk - kp_base] = p;
+      plan[rk] = p;
+    }
+    const int tot = ss.rank + __popcll(mask);
+    if (tot > hi) break;  // the chunk reaches past this tile: keep it for the next one
+    ss.rank = tot;
+    ss.p0 += 64;
+  }
+  fence_wave();
+}
+
+// Total kept positions of the window (for the DSA_FLAG_COUNT check).
+__device__ int count_kept(const SkipSet& ss, int lane) {
+  int n = 0;
+  for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64) n += __popcll(__ballot(is_kept(ss, p0 + lane)));
+  return n;
+}
+
+template <int D, int G, int U, bool FUSED>
 __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   constexpr int LPR = D / 8;       // lanes per row
   constexpr int RPI = 64 / LPR;    // rows per load instruction
-  constexpr int RPB = RPI * U;     // rows per wave block
+  constexpr int T = RPI * U;       // rows per wave tile (<= 64)
+  static_assert(T <= 64, "one kept position per lane");
+  constexpr int KS = FUSED ? kMaxFusedSplit : 1;
   __shared__ float red[kWaves][G][D + 2];
+  __shared__ float wl_s[G][KS];    // fused: window logits of the split
+  __shared__ int kp_s[KS];         // fused: kept positions of the split
+  extern __shared__ uint32_t bm_all[];  // fused: one skip bitmap per wave
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
   const int rg = lane / LPR;       // row group within the wave
   const int c = lane % LPR;        // 8-element column chunk
   const int s = blockIdx.x % a.S;
@@ -62,57 +190,79 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   const int kvh = pair % a.Hkv;
   const int b = pair / a.Hkv;
 
-  const RowRange rr = row_range(a, b, pair);
+  const RowRange rr = row_range<FUSED>(a, b, pair);
   const int n = rr.n;
   const int r0 = s * a.C;
   if (s > 0 && r0 >= n) return;
   const int r1 = min(n, r0 + a.C);
   const int nsplit = (n + a.C - 1) / a.C;
+  const bool dense = a.mode == DSA_MODE_DENSE;
+  const int w0 = max(r0, a.Lp) - a.Lp;  // first window rank of the split
 
   const int64_t base = (a.row_base ? a.row_base[b] : static_cast<int64_t>(b) * a.sb) +
                        static_cast<int64_t>(kvh) * a.sh + c * 8;
   const uint16_t* kb = a.k + base;
   const uint16_t* vb = a.v + base;
-  const int32_t* idx = a.idx + static_cast<size_t>(pair) * a.plan_cap;
-  const bool dense = a.mode == DSA_MODE_DENSE;
+  const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
+
+  uint4 qr[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+    qr[g] = *reinterpret_cast<const uint4*>(
+        a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
+
+  SkipSet ss{};
+  bool have_set = false;
+  if constexpr (FUSED) {
+    // A wave owns kept decode rows if one of its tiles reaches past the prompt.
+    const int first = r0 + wave * T;
+    bool owns = false;
+    if (first < r1 && r1 > a.Lp) {
+      const int last = first + (r1 - 1 - first) / (nwaves * T) * (nwaves * T);
+      owns = last + T > a.Lp;
+    }
+    // Split 0's first wave also rebuilds the set to report the plan flags.
+    if (owns || (s == 0 && wave == 0 && rr.t >= 0)) {
+      build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, ss);
+      have_set = true;
+    }
+  }
 
   float qf[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const uint4 qr = *reinterpret_cast<const uint4*>(
-        a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
-    unpack8(qr, qf[g]);
-  }
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
+    unpack8(qr[g], qf[g]);
     m[g] = kNegBig;
     l[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   }
 
-  for (int blk = r0 + wave * RPB; blk < r1; blk += kWaves * RPB) {
-    int crow[U];
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = blk + u * RPI + rg;
-      ok[u] = r < r1;
-      int cr = r;
-      if (ok[u] && !dense && r >= a.Lp) cr = a.Lp + min(max(idx[r - a.Lp], 0), rr.t);
-      crow[u] = ok[u] ? cr : 0;
+  for (int rs = r0 + wave * T; rs < r1; rs += nwaves * T) {
+    // Kept positions of the tile's window rows: lane i holds row rs + i.
+    int pos_l = 0;
+    const bool has_win = !dense && rs + T > a.Lp;
+    if (has_win) {
+      if constexpr (FUSED) {
+        const int lo = max(rs, a.Lp) - a.Lp, hi = min(rs + T, r1) - a.Lp;
+        rank_window(a, pair, lane, ss, lo, hi, kp_s, w0);
+        const int r = rs + lane;
+        if (lane < T && r < r1 && r >= a.Lp) pos_l = kp_s[r - a.Lp - w0];
+      } else {
+        const int r = rs + lane;
+        if (lane < T && r < r1 && r >= a.Lp) pos_l = min(max(widx[r], 0), rr.t);
+      }
     }
     uint4 kr[U], vr[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      kr[u] = make_uint4(0, 0, 0, 0);
-      if (ok[u]) kr[u] = *reinterpret_cast<const uint4*>(kb + crow[u] * a.sr);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      vr[u] = make_uint4(0, 0, 0, 0);
-      if (ok[u]) vr[u] = *reinterpret_cast<const uint4*>(vb + crow[u] * a.sr);
+      const int r = rs + u * RPI + rg;
+      const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
+      int cr = 0;  // rows past the split end read row 0 and get weight 0
+      if (r < r1) cr = (dense || r < a.Lp) ? r : a.Lp + wpos;
+      kr[u] = *reinterpret_cast<const uint4*>(kb + cr * a.sr);
+      vr[u] = *reinterpret_cast<const uint4*>(vb + cr * a.sr);
     }
 
     float sc[U][G];
@@ -128,15 +278,19 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
         sc[u][g] = group_sum<LPR>(x);
       }
     }
-    if (a.wlog) {
+    if (has_win && c == 0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int r = blk + u * RPI + rg;
-        if (ok[u] && c == 0 && r >= a.Lp) {
+        const int r = rs + u * RPI + rg;
+        if (r < r1 && r >= a.Lp) {
 #pragma unroll
-          for (int g = 0; g < G; ++g)
-            a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (r - a.Lp)] =
-                sc[u][g] * a.scale;
+          for (int g = 0; g < G; ++g) {
+            const float logit = sc[u][g] * a.scale;
+            if (a.wlog)
+              a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (r - a.Lp)] =
+                  logit;
+            if constexpr (FUSED) wl_s[g][r - a.Lp - w0] = logit;
+          }
         }
       }
     }
@@ -145,8 +299,8 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
       float mx = kNegBig;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        sc[u][g] *= a.scale_log2;
-        if (ok[u]) mx = fmaxf(mx, sc[u][g]);
+        sc[u][g] = rs + u * RPI + rg < r1 ? sc[u][g] * a.scale_log2 : kNegBig;
+        mx = fmaxf(mx, sc[u][g]);
       }
       const float mnew = fmaxf(m[g], mx);
       const float alpha = fast_exp2(m[g] - mnew);
@@ -159,12 +313,32 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     for (int u = 0; u < U; ++u) {
       float vf[8];
       unpack8(vr[u], vf);
+      const bool ok = rs + u * RPI + rg < r1;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        const float p = ok[u] ? fast_exp2(sc[u][g] - m[g]) : 0.f;
+        const float p = ok ? fast_exp2(sc[u][g] - m[g]) : 0.f;
         l[g] += p;
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+      }
+    }
+  }
+
+  if constexpr (FUSED) {
+    // Split 0 reports the plan's count and flags, as dsa_plan would.
+    if (s == 0 && wave == 0 && lane == 0 && rr.t < 0) {
+      a.plan_count[pair] = 0;
+      a.plan_flags[pair] = rr.flags;
+    }
+    if (s == 0 && wave == 0 && have_set) {
+      int flags = rr.flags | ss.flags;
+      const int kept = count_kept(ss, lane);
+      if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
+          kept != min(rr.t + 1, a.Natt))
+        flags |= DSA_FLAG_COUNT;
+      if (lane == 0) {
+        a.plan_count[pair] = n - a.Lp;
+        a.plan_flags[pair] = flags;
       }
     }
   }
@@ -200,17 +374,37 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
+
+  if constexpr (FUSED) {
+    // Phase-2 selection, when this workgroup saw every kept window key.
+    if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr - 2) {
+      const int k = rr.t - (a.Natt - 1);
+      if (k < a.state_cap) {
+        const int cnt = a.st_count[pair];
+        if (cnt < k) {
+          if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
+        } else {
+          const int nwin = n - a.Lp;
+          int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl_s[g][j]; });
+          if (lane == 0) {
+            if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
+            const int d = min(max(rr.t - kp_s[jbest], 0), a.Nr - 2);
+            a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
+            a.st_count[pair] = k + 1;
+          }
+        }
+      }
+    }
+  }
   if (wave != 0) return;
 
-  // Merge the 4 waves; lane j handles columns j and j + 64.
+  // Merge the waves; lane j handles columns j and j + 64.
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     float M = kNegBig;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red[w][g][D]);
+    for (int w = 0; w < nwaves; ++w) M = fmaxf(M, red[w][g][D]);
     float L = 0.f, A0 = 0.f, A1 = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
+    for (int w = 0; w < nwaves; ++w) {
       const float sw = fast_exp2(red[w][g][D] - M);
       L += red[w][g][D + 1] * sw;
       A0 += red[w][g][lane] * sw;
@@ -234,29 +428,21 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   }
 }
 
-// One wave per (request, query head): out = sum_s e^{m_s - M} acc_s /
-// sum_s e^{m_s - M} l_s over the request's splits (base-2 exponents, as the
-// partial maxima are kept in log2 units).
+// out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s over the splits of
+// (request b, query head g of KV head kvh), in base-2 exponents (the partial
+// maxima are kept in log2 units).  Called by one wave.
 template <int D>
-__global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
-  const int lane = threadIdx.x & 63;
-  const int bh = blockIdx.x * kWaves + (threadIdx.x >> 6);
-  if (bh >= a.B * a.Hq) return;
-  const int b = bh / a.Hq;
-  const int h = bh % a.Hq;
-  const int kvh = h / G;
-  const int g = h % G;
+__device__ __forceinline__ void combine_one(const DecodeArgs& a, int lane, int b, int kvh, int g,
+                                            int G, int nsplit) {
   const int pair = b * a.Hkv + kvh;
-  const RowRange rr = row_range(a, b, pair);
-  const int nsplit = (rr.n + a.C - 1) / a.C;
-  if (nsplit <= 1) return;
   const float* pp = a.part + (static_cast<size_t>(pair) * a.S * G + g) * (D + 2);
   const size_t sstride = static_cast<size_t>(G) * (D + 2);
   float M = kNegBig;
   for (int s = lane; s < nsplit; s += 64) M = fmaxf(M, pp[s * sstride + D]);
   M = wave_max(M);
   float L = 0.f;
-  for (int s = lane; s < nsplit; s += 64) L += pp[s * sstride + D + 1] * fast_exp2(pp[s * sstride + D] - M);
+  for (int s = lane; s < nsplit; s += 64)
+    L += pp[s * sstride + D + 1] * fast_exp2(pp[s * sstride + D] - M);
   L = wave_sum(L);
   float A0 = 0.f, A1 = 0.f;
   for (int s = 0; s < nsplit; ++s) {
@@ -265,39 +451,116 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
     if constexpr (D == 128) A1 += pp[s * sstride + lane + 64] * sw;
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  float* o = a.out + static_cast<size_t>(bh) * D;
+  float* o = a.out + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D;
   o[lane] = A0 * inv;
   if constexpr (D == 128) o[lane + 64] = A1 * inv;
 }
 
+// One wave per (request, query head).
+template <int D>
+__global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
+  const int lane = threadIdx.x & 63;
+  const int bh = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (bh >= a.B * a.Hq) return;
+  const int b = bh / a.Hq;
+  const int h = bh % a.Hq;
+  const RowRange rr = row_range<false>(a, b, b * a.Hkv + h / G);
+  const int nsplit = (rr.n + a.C - 1) / a.C;
+  if (nsplit <= 1) return;
+  combine_one<D>(a, lane, b, h / G, h % G, G, nsplit);
+}
+
+// Fused step, several splits: one wave per (request, KV head) merges the
+// splits of every query head of the group, then runs the phase-2 selection
+// on the window logits and the plan the split workgroups wrote.
 template <int D, int G>
-hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st) {
+__global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int pair = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (pair >= a.B * a.Hkv) return;
+  const int b = pair / a.Hkv;
+  const int kvh = pair % a.Hkv;
+  const RowRange rr = row_range<true>(a, b, pair);
+  const int nsplit = (rr.n + a.C - 1) / a.C;
+  if (nsplit <= 1) return;
+#pragma unroll
+  for (int g = 0; g < G; ++g) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
+  const int t = rr.t;
+  if (t < a.Natt - 1 || t > a.Nr - 2) return;
+  const int k = t - (a.Natt - 1);
+  if (k >= a.state_cap) return;
+  const int cnt = a.st_count[pair];
+  if (cnt < k) {
+    if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
+    return;
+  }
+  const int nwin = rr.n - a.Lp;
+  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap;
+  const int plan_cap = a.plan_cap;
+  int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl[g * plan_cap + j]; });
+  if (lane == 0) {
+    if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
+    const int pos = a.plan_idx[static_cast<size_t>(pair) * a.plan_cap + jbest];
+    const int d = min(max(t - pos, 0), a.Nr - 2);
+    a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
+    a.st_count[pair] = k + 1;
+  }
+}
+
+template <int D, int G, int U, bool FUSED>
+void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                  hipEvent_t t1) {
   const int grid = d.B * d.Hkv * d.S;
-  if (d.U >= 4)
-    decode_kernel<D, G, 4><<<grid, kBlock, 0, st>>>(a);
+  const int block = 64 * d.NW;
+  const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * d.NW * a.words) : 0u;
+  if (t0 || t1)
+    hipExtLaunchKernelGGL(decode_kernel<D, G, U, FUSED>, dim3(grid), dim3(block), lds, st, t0, t1,
+                          0, a);
   else
-    decode_kernel<D, G, 2><<<grid, kBlock, 0, st>>>(a);
+    decode_kernel<D, G, U, FUSED><<<grid, block, lds, st>>>(a);
+}
+
+template <int D, int G, bool FUSED>
+hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                     hipEvent_t t1) {
+  switch (d.U) {
+    case 8: launch_split<D, G, 8, FUSED>(d, a, st, t0, t1); break;
+    case 4: launch_split<D, G, 4, FUSED>(d, a, st, t0, t1); break;
+    default: launch_split<D, G, 2, FUSED>(d, a, st, t0, t1); break;
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || d.S <= 1) return e;
-  const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
-  combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
+  if (FUSED) {
+    const int cgrid = (d.B * d.Hkv + kWaves - 1) / kWaves;
+    combine_select_kernel<D, G><<<cgrid, kBlock, 0, st>>>(a);
+  } else {
+    const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
+    combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
+  }
   return hipGetLastError();
 }
 
-template <int D>
-hipError_t launch_d(const Derived& d, const DecodeArgs& a, hipStream_t st) {
+template <int D, bool FUSED>
+hipError_t launch_d(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                    hipEvent_t t1) {
   switch (d.G) {
-    case 1: return launch_dg<D, 1>(d, a, st);
-    case 2: return launch_dg<D, 2>(d, a, st);
-    case 4: return launch_dg<D, 4>(d, a, st);
-    default: return launch_dg<D, 8>(d, a, st);
+    case 1: return launch_dg<D, 1, FUSED>(d, a, st, t0, t1);
+    case 2: return launch_dg<D, 2, FUSED>(d, a, st, t0, t1);
+    case 4: return launch_dg<D, 4, FUSED>(d, a, st, t0, t1);
+    default: return launch_dg<D, 8, FUSED>(d, a, st, t0, t1);
   }
 }
 
 }  // namespace
 
-hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st) {
-  return d.D == 64 ? launch_d<64>(d, a, st) : launch_d<128>(d, a, st);
+hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                         hipEvent_t t1) {
+  return d.D == 64 ? launch_d<64, false>(d, a, st, t0, t1) : launch_d<128, false>(d, a, st, t0, t1);
+}
+
+hipError_t launch_step(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                       hipEvent_t t1) {
+  return d.D == 64 ? launch_d<64, true>(d, a, st, t0, t1) : launch_d<128, true>(d, a, st, t0, t1);
 }
 
 }  // namespace dsa

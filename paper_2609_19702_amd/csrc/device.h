@@ -63,3 +63,57 @@ __device__ __forceinline__ float wave_sum(float x) {
 }
 
 }  // namespace dsa
+
+namespace dsa {
+
+// (value, index) minimum with ties to the smaller index.
+__device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2) {
+  if (v2 < v || (v2 == v && j2 < j)) {
+    v = v2;
+    j = j2;
+  }
+}
+
+// Phase-2 selection score argmin of one KV head over its n kept window keys
+// (section 4, Algorithm 1): logit(g, j) is sm_scale * q_g . k_j of query head
+// g of the group for window key j.  Group size 1 takes the argmin of the
+// logits (the softmax orders them identically); larger groups sum the
+// group's window softmaxes.  Ties go to the smallest j (the oldest key).
+// Called by a whole wave; every lane returns the same index (or a value
+// outside [0, n) only if every score is NaN).
+template <int G, typename Logit>
+__device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
+  float best = __builtin_inff();
+  int jbest = 0x7fffffff;
+  if constexpr (G == 1) {
+    for (int j = lane; j < n; j += 64) argmin_merge(best, jbest, logit(0, j), j);
+  } else {
+    float mx[G], inv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float m = -__builtin_inff();
+      for (int j = lane; j < n; j += 64) m = fmaxf(m, logit(g, j));
+      m = wave_max(m);
+      float s = 0.f;
+      for (int j = lane; j < n; j += 64) s += __expf(logit(g, j) - m);
+      s = wave_sum(s);
+      mx[g] = m;
+      inv[g] = 1.f / s;
+    }
+    for (int j = lane; j < n; j += 64) {
+      float sigma = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) sigma += __expf(logit(g, j) - mx[g]) * inv[g];
+      argmin_merge(best, jbest, sigma, j);
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float v2 = __shfl_xor(best, m, 64);
+    const int j2 = __shfl_xor(jbest, m, 64);
+    argmin_merge(best, jbest, v2, j2);
+  }
+  return jbest;
+}
+
+}  // namespace dsa

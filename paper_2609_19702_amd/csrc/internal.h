@@ -23,6 +23,7 @@ struct Derived {
   int U;          // loads in flight per wave per operand (unroll)
   int C;          // rows per split workgroup
   int S;          // splits per (request, KV head), upper bound
+  int NW;         // waves per decode workgroup (1..kWaves)
   size_t ws_bytes;
 };
 
@@ -30,6 +31,8 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 
 constexpr int kWaves = 4;          // waves per workgroup in every kernel
 constexpr int kBlock = 64 * kWaves;
+constexpr int kMaxFusedSplit = 256;  // rows per diagonal-mode split (fused step keeps them in LDS)
+constexpr int kMaxFusedWindow = 16384;  // N_r of the fused step (skip bitmap per wave in LDS)
 constexpr float kNegBig = -1.0e30f;  // "no score yet": finite, so exp2 of a difference is 0
 
 struct PlanArgs {
@@ -57,6 +60,14 @@ struct DecodeArgs {
   float* wlog;           // window logits or nullptr
   float* part;           // split partials (S > 1)
   int B, Hq, Hkv, Lp, Ldec, mode, plan_cap, C, S;
+  // fused step only: selection state (in/out) and plan (out)
+  int32_t* st_count;
+  int32_t* st_flags;
+  uint16_t* st_off;
+  int32_t* plan_count;
+  int32_t* plan_flags;
+  int32_t* plan_idx;
+  int Nr, Natt, state_cap, words;
 };
 
 struct SelectArgs {
@@ -78,7 +89,10 @@ struct ResetArgs {
 };
 
 hipError_t launch_plan(const Derived& d, const PlanArgs& a, hipStream_t st);
-hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st);
+hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st,
+                         hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+hipError_t launch_step(const Derived& d, const DecodeArgs& a, hipStream_t st,
+                       hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_select(const Derived& d, const SelectArgs& a, hipStream_t st);
 hipError_t launch_reset(const Derived& d, const ResetArgs& a, hipStream_t st);
 

@@ -22,9 +22,22 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
   const bool live = pair < a.pairs;
   uint32_t* bm = bitmap_all + wave * a.words;
 
-  int t = -1, flags = 0, nuse = 0;
+  // Every load of the wave is issued before any of them is used: the
+  // decode position, the stored count and the first kPre*64 stored offsets
+  // (entries past the count are ignored).
+  const bool diag = a.mode == DSA_MODE_DIAGONAL;
+  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
+  int t = live ? a.pos[pair / a.Hkv] : -1;
+  const int cnt = (live && diag) ? a.st_count[pair] : 0;
+  constexpr int kPre = 8;
+  int dv[kPre];
+#pragma unroll
+  for (int i = 0; i < kPre; ++i) {
+    const int e = lane + 64 * i;
+    dv[i] = (live && diag && e < a.state_cap) ? off[e] : 0;
+  }
+  int flags = 0, nuse = 0;
   if (live) {
-    t = a.pos[pair / a.Hkv];
     if (t < 0) {
       flags = DSA_FLAG_INACTIVE;
     } else if (t >= a.Ldec) {
@@ -32,10 +45,8 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
       flags = DSA_FLAG_POS_CLAMPED;
     }
   }
-  const bool diag = a.mode == DSA_MODE_DIAGONAL;
   if (live && diag && t >= 0) {
     const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
-    const int cnt = a.st_count[pair];
     if (cnt < nvalid) flags |= DSA_FLAG_STATE_BEHIND;
     nuse = min(max(cnt, 0), nvalid);
   }
@@ -45,14 +56,17 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
   __syncthreads();
   if (diag && live && t >= 0) {
     bool bad = false;
-    const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-    for (int e = lane; e < nuse; e += 64) {
-      const int d = off[e];
-      if (d <= a.Nr - 2) {
-        atomicOr(&bm[d >> 5], 1u << (d & 31));
-      } else {
-        bad = true;
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int e = lane + 64 * i;
+      if (e < nuse) {
+        const int d = dv[i];
+        if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
       }
+    }
+    for (int e = lane + 64 * kPre; e < nuse; e += 64) {
+      const int d = off[e];
+      if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
     }
     if (__ballot(bad)) flags |= DSA_FLAG_BAD_OFFSET;
   }

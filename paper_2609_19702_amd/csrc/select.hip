@@ -14,23 +14,6 @@
 namespace dsa {
 namespace {
 
-// (value, index) minimum with ties to the smaller index.
-__device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2) {
-  if (v2 < v || (v2 == v && j2 < j)) {
-    v = v2;
-    j = j2;
-  }
-}
-
-__device__ __forceinline__ void wave_argmin(float& v, int& j) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const float v2 = __shfl_xor(v, m, 64);
-    const int j2 = __shfl_xor(j, m, 64);
-    argmin_merge(v, j, v2, j2);
-  }
-}
-
 template <int G>
 __global__ __launch_bounds__(kBlock) void select_kernel(SelectArgs a) {
   const int lane = threadIdx.x & 63;
@@ -39,48 +22,21 @@ __global__ __launch_bounds__(kBlock) void select_kernel(SelectArgs a) {
   const int b = pair / a.Hkv;
   const int kvh = pair % a.Hkv;
   int t = a.pos[b];
+  const int cnt = a.st_count[pair];
+  const int n = min(max(a.count[pair], 0), a.plan_cap);
   if (t < 0) return;
   t = min(t, a.Ldec - 1);
   if (t < a.Natt - 1 || t > a.Nr - 2) return;
   const int k = t - (a.Natt - 1);
   if (k >= a.state_cap) return;
-  const int cnt = a.st_count[pair];
   if (cnt < k) {
     if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
     return;
   }
-  const int n = min(max(a.count[pair], 0), a.plan_cap);
   if (n == 0) return;
   const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap;
-
-  float best = __builtin_inff();
-  int jbest = 0x7fffffff;
-  if constexpr (G == 1) {
-    for (int j = lane; j < n; j += 64) argmin_merge(best, jbest, wl[j], j);
-  } else {
-    // sigma_j = sum_g exp(s_gj - max_g) / sum_j' exp(s_gj' - max_g)
-    float mx[G], inv[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float* w = wl + static_cast<size_t>(g) * a.plan_cap;
-      float m = -__builtin_inff();
-      for (int j = lane; j < n; j += 64) m = fmaxf(m, w[j]);
-      m = wave_max(m);
-      float s = 0.f;
-      for (int j = lane; j < n; j += 64) s += __expf(w[j] - m);
-      s = wave_sum(s);
-      mx[g] = m;
-      inv[g] = 1.f / s;
-    }
-    for (int j = lane; j < n; j += 64) {
-      float sigma = 0.f;
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-        sigma += __expf(wl[static_cast<size_t>(g) * a.plan_cap + j] - mx[g]) * inv[g];
-      argmin_merge(best, jbest, sigma, j);
-    }
-  }
-  wave_argmin(best, jbest);
+  const int plan_cap = a.plan_cap;
+  int jbest = window_argmin<G>(lane, n, [&](int g, int j) { return wl[g * plan_cap + j]; });
   if (lane == 0) {
     if (jbest < 0 || jbest >= n) jbest = 0;  // only for NaN logits
     const int pos = a.idx[static_cast<size_t>(pair) * a.plan_cap + jbest];

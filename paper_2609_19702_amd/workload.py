@@ -94,28 +94,27 @@ def build_histories(bt: Batch, device="cuda"):
 def sparse_layer(bt: Batch, L: Layer, timer=None):
     p, s = bt.p, bt.s
     B.plan(p, s, bt.pos, L.bufs.state, L.bufs.plan)
-    if timer is not None:
-        timer[0].record()
     B.decode_attention(p, s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, L.bufs.plan,
-                       bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace)
-    if timer is not None:
-        timer[1].record()
+                       bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace, events=timer)
     B.select(p, s, bt.pos, L.bufs.plan, L.bufs.logits, L.bufs.state)
+
+
+def fused_layer(bt: Batch, L: Layer, timer=None):
+    B.decode_step(bt.p, bt.s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, L.bufs.state,
+                  L.bufs.plan, bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace, events=timer)
 
 
 def dense_layer(bt: Batch, L: Layer, timer=None):
     db = bt.dense_bufs
-    if timer is not None:
-        timer[0].record()
     B.decode_attention(bt.pd, bt.s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, None,
-                       bt.scale, db.out, None, db.workspace)
-    if timer is not None:
-        timer[1].record()
+                       bt.scale, db.out, None, db.workspace, events=timer)
 
 
-def step(bt: Batch, dense: bool = False, timers=None):
-    """One decode step over all layers; ``timers[i]`` (a pair of events) is
-    recorded around layer i's attention launch when given."""
-    fn = dense_layer if dense else sparse_layer
+def step(bt: Batch, dense: bool = False, timers=None, fused: bool = False):
+    """One decode step over all layers: dense mode, the three separate calls
+    (plan, decode, select) or the fused step.  ``timers[i]`` (a pair from
+    ``binding.timing_events``) receives the start and end of layer i's
+    split-K decode kernel when given."""
+    fn = dense_layer if dense else (fused_layer if fused else sparse_layer)
     for i, L in enumerate(bt.layers):
         fn(bt, L, None if timers is None else timers[i])

@@ -45,8 +45,14 @@ def test_fullsize_sampled_parity(name):
     bt = workload.make_batch(w, layers=1)
     workload.build_histories(bt)
     L = bt.layers[0]
+    state0 = L.bufs.state.clone()
     workload.sparse_layer(bt, L)
     sparse_out = L.bufs.out.cpu().numpy().astype(np.float64)
+    # the fused step reproduces the separate calls bit for bit at full size
+    ref = (L.bufs.out.clone(), L.bufs.state.clone())
+    L.bufs.state.copy_(state0)
+    workload.fused_layer(bt, L)
+    assert torch.equal(L.bufs.out, ref[0]) and torch.equal(L.bufs.state, ref[1])
     workload.dense_layer(bt, L)
     dense_out = bt.dense_bufs.out.cpu().numpy().astype(np.float64)
     torch.cuda.synchronize()
