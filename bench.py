@@ -48,6 +48,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--only", default=None, choices=["fused", "separate", "dense"],
+                    help="time one step variant only (shorter profiler runs)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
+                    help="run a plain device copy of MB megabytes 10 times and exit (the "
+                         "reference for scaling the profiler's FETCH_SIZE/WRITE_SIZE)")
     return ap.parse_args()
 
 
@@ -175,6 +180,15 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     B.lib()
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "launches": 10}))
+        return
     w = synth.WORKLOADS[args.workload]
     if args.positions:
         w = w.with_(positions=args.positions)
@@ -185,7 +199,7 @@ def main():
     print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
           f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
 
-    modes = ("fused", "separate", "dense")
+    modes = (args.only,) if args.only else ("fused", "separate", "dense")
     for _ in range(args.warmup):
         for mode in modes:
             run_step(bt, mode)
@@ -197,6 +211,10 @@ def main():
     torch.cuda.synchronize()
     ms = {m: timed_steps(bt, args.steps, m, graphs[m]) for m in modes}
     launch = {m: kernel_times(bt, args.steps, m) for m in modes}
+    if args.only:
+        print(json.dumps({"only": args.only, "ms_per_step": ms[args.only],
+                          "decode_launch_us": statistics.fmean(launch[args.only]) * 1e3}))
+        return
     ms_sparse, ms_dense = ms["fused"], ms["dense"]
     launch_sparse, launch_dense = launch["fused"], launch["dense"]
     print(f"# ms/step ({'eager' if args.eager else 'graph'}): "

@@ -8,7 +8,7 @@ decode positions whose KV has been evicted.  No reformulation (offsets,
 bitmaps) is used here; the tests compare this literal form against other
 formulations.
 
-Readings of the paper taken here (each is listed in the design doc):
+Readings of the paper taken here:
 
 * Phase boundaries follow the algorithm box: phase 1 while ``t < N_att-1``,
   phase 2 while ``t < N_r``, phase 3 afterwards.  The prose sentence that

@@ -70,7 +70,7 @@ class StateLayout(C.Structure):
 class LaunchInfo(C.Structure):
     _fields_ = [("rows_per_split", C.c_int32), ("max_splits", C.c_int32),
                 ("workgroups", C.c_int32), ("kernel_variant", C.c_int32),
-                ("workspace_bytes", C.c_size_t)]
+                ("waves_per_group", C.c_int32), ("workspace_bytes", C.c_size_t)]
 
 
 # name -> (restype, argtypes); mirrors include/dsa.h

@@ -102,7 +102,18 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   if (pairs * S > (int64_t(1) << 31) - 1) return DSA_ERR_INVALID_ARG;
   d->C = static_cast<int>(C);
   d->S = static_cast<int>(S);
-  d->NW = static_cast<int>(std::min<int64_t>(kWaves, (C + block_rows - 1) / block_rows));
+  // Waves per workgroup: the most tiles any split has (tiles stop at the
+  // prompt/decode boundary, so a split can have one more than C / tile).
+  int64_t max_tiles = 1;
+  for (int64_t sp = 0; sp < S; ++sp) {
+    const int64_t r0 = sp * C, r1 = std::min(rows_max, r0 + C);
+    const int64_t pe = std::min<int64_t>(r1, d->Lp);
+    const int64_t wst = std::max<int64_t>(r0, d->Lp);
+    const int64_t tiles = (pe > r0 ? (pe - r0 + block_rows - 1) / block_rows : 0) +
+                          (r1 > wst ? (r1 - wst + block_rows - 1) / block_rows : 0);
+    max_tiles = std::max(max_tiles, tiles);
+  }
+  d->NW = static_cast<int>(std::min<int64_t>(kWaves, max_tiles));
   d->ws_bytes = S > 1 ? static_cast<size_t>(pairs) * S * G * (d->D + 2) * sizeof(float) : 0;
   return DSA_OK;
 }
@@ -184,6 +195,7 @@ DSA_API dsa_status dsa_get_launch_info(const dsa_params* p, const dsa_shape* s,
   out->max_splits = d.S;
   out->workgroups = d.B * d.Hkv * d.S;
   out->kernel_variant = d.U;
+  out->waves_per_group = d.NW;
   out->workspace_bytes = d.ws_bytes;
   return DSA_OK;
 }

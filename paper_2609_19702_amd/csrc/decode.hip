@@ -18,10 +18,12 @@
 //     every K and V load of a tile before using any of them; rows past the
 //     end of the split read a valid row and get weight 0, so no load sits
 //     behind a branch;
+//   - tiles hold either prompt rows or kept decode rows, never both; the
+//     kept positions of a window tile are held one per lane and handed to
+//     the row groups with ds_bpermute, prompt tiles need none;
+//   - K/V rows are loaded with the non-temporal hint (streamed once);
 //   - a workgroup has as many waves (1..4) as its split has tiles, so no wave
 //     sits idle holding registers;
-//   - the kept positions of a tile are held one per lane and handed to the
-//     row groups with ds_bpermute; tiles made only of prompt rows need none;
 //   - q.k partial sums are reduced inside the row's lane group with DPP row
 //     permutations (no LDS);
 //   - softmax runs online in fp32 (base-2 exponent with the scale folded
@@ -33,7 +35,9 @@
 // The fused step (FUSED = true, diagonal mode) reads the selection state
 // instead of a plan: each wave that owns kept decode rows rebuilds the skip
 // set of its (request, KV head) as a bitmap in its own LDS slice and ranks the
-// window positions with ballots, writing the plan as a by-product; when one
+// window positions with ballots, writing the plan as a by-product, before
+// any wave of the workgroup starts loading K/V (the workgroup then streams
+// all its rows together rather than the kept rows trailing); when one
 // split covers the whole (request, KV head) the same workgroup then runs the
 // phase-2 argmin on the window logits it computed and appends the skip entry.
 // Every value it produces is bit-identical to dsa_plan -> dsa_decode_attention
@@ -93,27 +97,37 @@ __device__ __forceinline__ void fence_wave() {
   __builtin_amdgcn_wave_barrier();
 }
 
-__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, uint32_t* bm,
-                               SkipSet& ss) {
-  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-  const int cnt = a.st_count[pair];
+// Stored count and the first kPre*64 stored offsets of a (request, KV
+// head), loaded into registers ahead of their use.
+struct StateRegs {
+  int cnt;
   int dv[kPre];
+};
+
+__device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, StateRegs& sr) {
+  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
+  sr.cnt = a.st_count[pair];
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
     const int e = lane + 64 * i;
-    dv[i] = e < a.state_cap ? off[e] : 0;
+    sr.dv[i] = e < a.state_cap ? off[e] : 0;
   }
+}
+
+__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, uint32_t* bm,
+                               const StateRegs& sr, SkipSet& ss) {
+  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
   for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
   const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
-  int flags = cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
-  const int nuse = min(max(cnt, 0), nvalid);
+  int flags = sr.cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
+  const int nuse = min(max(sr.cnt, 0), nvalid);
   fence_wave();
   bool bad = false;
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
     const int e = lane + 64 * i;
     if (e < nuse) {
-      const int d = dv[i];
+      const int d = sr.dv[i];
       if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
     }
   }
@@ -211,21 +225,45 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     qr[g] = *reinterpret_cast<const uint4*>(
         a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
 
+  // Tiles never straddle the prompt/decode boundary: the split's prompt rows
+  // [r0, pe) and decode rows [wst, r1) are each cut into tiles of T rows,
+  // tile j going to wave j % nwaves.  Prompt tiles and dense-mode decode
+  // tiles load at once; diagonal-mode decode tiles wait for their kept
+  // positions.  (Both modes cut the same way, so with nothing skipped they
+  // add the same numbers in the same order.)
+  const int pe = min(r1, a.Lp);
+  const int wst = max(r0, a.Lp);
+  const int P = pe > r0 ? (pe - r0 + T - 1) / T : 0;
+  const int Wn = r1 > wst ? (r1 - wst + T - 1) / T : 0;
+
   SkipSet ss{};
+  StateRegs sreg{};
   bool have_set = false;
+  // The wave holding window rank 0 (the first decode tile of the pair)
+  // reports the plan's count and flags, as dsa_plan would.
+  bool reporter = false;
   if constexpr (FUSED) {
-    // A wave owns kept decode rows if one of its tiles reaches past the prompt.
-    const int first = r0 + wave * T;
-    bool owns = false;
-    if (first < r1 && r1 > a.Lp) {
-      const int last = first + (r1 - 1 - first) / (nwaves * T) * (nwaves * T);
-      owns = last + T > a.Lp;
+    // First window tile of this wave, if it has one.
+    const int j0 = P + ((wave - P) % nwaves + nwaves) % nwaves;
+    if (j0 < P + Wn) load_state(a, pair, lane, sreg);
+    reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && j0 == P);
+  }
+
+  if constexpr (FUSED) {
+    // Rank every kept window row this wave owns before any wave of the
+    // workgroup loads K/V: the whole workgroup then streams its rows
+    // together instead of the window rows queueing behind the prompt rows.
+    for (int j = wave; j < P + Wn; j += nwaves) {
+      if (j < P) continue;
+      const int rs = wst + (j - P) * T;
+      const int re = min(rs + T, r1);
+      if (!have_set) {
+        build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
+        have_set = true;
+      }
+      rank_window(a, pair, lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
     }
-    // Split 0's first wave also rebuilds the set to report the plan flags.
-    if (owns || (s == 0 && wave == 0 && rr.t >= 0)) {
-      build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, ss);
-      have_set = true;
-    }
+    if (Wn > 0) __syncthreads();
   }
 
   float qf[G][8];
@@ -239,19 +277,18 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   }
 
-  for (int rs = r0 + wave * T; rs < r1; rs += nwaves * T) {
-    // Kept positions of the tile's window rows: lane i holds row rs + i.
+  for (int j = wave; j < P + Wn; j += nwaves) {
+    const bool dec = j >= P;
+    const bool has_win = dec && !dense;
+    const int rs = dec ? wst + (j - P) * T : r0 + j * T;
+    const int re = min(rs + T, dec ? r1 : pe);
+    // Kept positions of a window tile: lane i holds row rs + i.
     int pos_l = 0;
-    const bool has_win = !dense && rs + T > a.Lp;
     if (has_win) {
       if constexpr (FUSED) {
-        const int lo = max(rs, a.Lp) - a.Lp, hi = min(rs + T, r1) - a.Lp;
-        rank_window(a, pair, lane, ss, lo, hi, kp_s, w0);
-        const int r = rs + lane;
-        if (lane < T && r < r1 && r >= a.Lp) pos_l = kp_s[r - a.Lp - w0];
+        if (lane < re - rs) pos_l = kp_s[rs + lane - a.Lp - w0];
       } else {
-        const int r = rs + lane;
-        if (lane < T && r < r1 && r >= a.Lp) pos_l = min(max(widx[r], 0), rr.t);
+        if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
       }
     }
     uint4 kr[U], vr[U];
@@ -259,10 +296,10 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     for (int u = 0; u < U; ++u) {
       const int r = rs + u * RPI + rg;
       const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
-      int cr = 0;  // rows past the split end read row 0 and get weight 0
-      if (r < r1) cr = (dense || r < a.Lp) ? r : a.Lp + wpos;
-      kr[u] = *reinterpret_cast<const uint4*>(kb + cr * a.sr);
-      vr[u] = *reinterpret_cast<const uint4*>(vb + cr * a.sr);
+      int cr = 0;  // rows past the tile end read row 0 and get weight 0
+      if (r < re) cr = has_win ? a.Lp + wpos : r;
+      kr[u] = load_stream16(kb + cr * a.sr);
+      vr[u] = load_stream16(vb + cr * a.sr);
     }
 
     float sc[U][G];
@@ -282,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int r = rs + u * RPI + rg;
-        if (r < r1 && r >= a.Lp) {
+        if (r < re) {
 #pragma unroll
           for (int g = 0; g < G; ++g) {
             const float logit = sc[u][g] * a.scale;
@@ -299,7 +336,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
       float mx = kNegBig;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        sc[u][g] = rs + u * RPI + rg < r1 ? sc[u][g] * a.scale_log2 : kNegBig;
+        sc[u][g] = rs + u * RPI + rg < re ? sc[u][g] * a.scale_log2 : kNegBig;
         mx = fmaxf(mx, sc[u][g]);
       }
       const float mnew = fmaxf(m[g], mx);
@@ -313,7 +350,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
     for (int u = 0; u < U; ++u) {
       float vf[8];
       unpack8(vr[u], vf);
-      const bool ok = rs + u * RPI + rg < r1;
+      const bool ok = rs + u * RPI + rg < re;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         const float p = ok ? fast_exp2(sc[u][g] - m[g]) : 0.f;
@@ -325,19 +362,17 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   }
 
   if constexpr (FUSED) {
-    // Split 0 reports the plan's count and flags, as dsa_plan would.
-    if (s == 0 && wave == 0 && lane == 0 && rr.t < 0) {
-      a.plan_count[pair] = 0;
-      a.plan_flags[pair] = rr.flags;
-    }
-    if (s == 0 && wave == 0 && have_set) {
-      int flags = rr.flags | ss.flags;
-      const int kept = count_kept(ss, lane);
-      if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
-          kept != min(rr.t + 1, a.Natt))
-        flags |= DSA_FLAG_COUNT;
+    if (reporter) {
+      int flags = rr.flags;
+      if (rr.t >= 0) {
+        flags |= ss.flags;
+        const int kept = count_kept(ss, lane);
+        if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
+            kept != min(rr.t + 1, a.Natt))
+          flags |= DSA_FLAG_COUNT;
+      }
       if (lane == 0) {
-        a.plan_count[pair] = n - a.Lp;
+        a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
         a.plan_flags[pair] = flags;
       }
     }

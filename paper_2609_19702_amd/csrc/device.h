@@ -22,6 +22,15 @@ __device__ __forceinline__ void unpack8(const uint4& r, float (&f)[8]) {
   f[7] = bf16_hi(r.w);
 }
 
+// 16-byte global load with the non-temporal hint: K/V rows are streamed once
+// per step, so they should not push the small per-step buffers (queries,
+// selection state, plans) out of the caches.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+  const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(x.x, x.y, x.z, x.w);
+}
+
 // DPP lane permutations inside a 16-lane row.
 constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]: lane ^ 1
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]: lane ^ 2
