@@ -156,7 +156,8 @@ typedef struct dsa_launch_info {
   int32_t rows_per_split;  /* C: keys per split workgroup                   */
   int32_t max_splits;      /* S: splits per (request, KV head) at most      */
   int32_t workgroups;      /* B * Hkv * S                                   */
-  int32_t kernel_variant;  /* loads in flight per wave and operand (unroll) */
+  int32_t kernel_variant;  /* K/V loads in flight per wave (2, 4 or 8), or 100 for
+                              the MFMA tile of grouped query heads (32 rows) */
   int32_t waves_per_group; /* waves per split workgroup (1..4)              */
   size_t workspace_bytes;  /* fp32 partials for the combine                 */
 } dsa_launch_info;

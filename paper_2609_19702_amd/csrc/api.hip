@@ -83,7 +83,10 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   const int u_default = G >= 8 ? 2 : (G >= 4 ? 4 : 8);
   const int u_env = env_int("DSA_TUNE_UNROLL", u_default);
   d->U = (u_env == 2 || u_env == 4 || u_env == 8) ? u_env : u_default;
-  const int block_rows = rows_per_instr * d->U;
+  // Grouped query heads take the MFMA tile (q.K^T on matrix cores) unless
+  // DSA_TUNE_VALU_GQA=1 asks for the vector-ALU tile.
+  d->MF = G >= 2 && env_int("DSA_TUNE_VALU_GQA", 0) != 1;
+  const int block_rows = d->MF ? kMfmaTile : rows_per_instr * d->U;
   const int64_t rows_max = d->Lp + (diag ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
   const int64_t split_bytes = env_int("DSA_TUNE_SPLIT_KB", 48) * int64_t(1024);
@@ -194,7 +197,7 @@ DSA_API dsa_status dsa_get_launch_info(const dsa_params* p, const dsa_shape* s,
   out->rows_per_split = d.C;
   out->max_splits = d.S;
   out->workgroups = d.B * d.Hkv * d.S;
-  out->kernel_variant = d.U;
+  out->kernel_variant = d.MF ? 100 : d.U;
   out->waves_per_group = d.NW;
   out->workspace_bytes = d.ws_bytes;
   return DSA_OK;

@@ -182,16 +182,129 @@ __device__ int count_kept(const SkipSet& ss, int lane) {
   return n;
 }
 
-template <int D, int G, int U, bool FUSED>
-__global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
-  constexpr int LPR = D / 8;       // lanes per row
+// One 32-row tile of the grouped-head path.  q.K^T runs on
+// v_mfma_f32_16x16x32_bf16: K rows are loaded straight into the A layout
+// (lane l: row l%16, 8 elements per k-step), the group's queries are the B
+// operand, and the C layout leaves head l%16's scores of rows 4*(l/16)+j in
+// lane l.  The softmax statistics stay in that layout; the weights reach the
+// V-layout lanes through a small LDS slice of the wave, and P.V runs in fp32
+// on the vector ALUs (bf16 weights would cost ~2^-9 relative error).
+template <int D, int G, bool FUSED>
+__device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs, int re,
+                                          bool has_win, int pos_l, const uint16_t* kmf,
+                                          const uint16_t* vb, const bf16x8* qb, int b, int kvh,
+                                          int w0, float& m_c, float& l_c, float (&acc)[G][8],
+                                          float* wls, float* ps, float* als) {
+  constexpr int LPR = D / 8, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
+  constexpr int NH = T / 16;  // 16-row MFMA blocks per tile
+  const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR;
+  uint4 kr[NH][NK];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    const int r = rs + 16 * h + lr;
+    const int wpos = has_win ? __shfl(pos_l, 16 * h + lr, 64) : 0;
+    int cr = 0;  // rows past the tile end read row 0 and get weight 0
+    if (r < re) cr = has_win ? a.Lp + wpos : r;
+#pragma unroll
+    for (int i = 0; i < NK; ++i) kr[h][i] = load_stream16(kmf + cr * a.sr + 32 * i);
+  }
+  uint4 vr[UV];
+#pragma unroll
+  for (int u = 0; u < UV; ++u) {
+    const int r = rs + u * RPI + rg;
+    const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
+    int cr = 0;
+    if (r < re) cr = has_win ? a.Lp + wpos : r;
+    vr[u] = load_stream16(vb + cr * a.sr);
+  }
+  f32x4 sc[NH];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    sc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NK; ++i)
+      sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[h][i]), qb[i],
+                                                      sc[h], 0, 0, 0);
+  }
+  if (has_win && lr < G) {
+#pragma unroll
+    for (int h = 0; h < NH; ++h)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = rs + 16 * h + 4 * lq + j;
+        if (r < re) {
+          const float logit = sc[h][j] * a.scale;
+          if (a.wlog)
+            a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + lr) * a.plan_cap + (r - a.Lp)] =
+                logit;
+          if constexpr (FUSED) wls[lr * kMaxFusedSplit + (r - a.Lp - w0)] = logit;
+        }
+      }
+  }
+  float s2[NH][4];
+  float mx = kNegBig;
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      s2[h][j] = rs + 16 * h + 4 * lq + j < re ? sc[h][j] * a.scale_log2 : kNegBig;
+      mx = fmaxf(mx, s2[h][j]);
+    }
+  mx = fmaxf(mx, shfl_xor(mx, 16));
+  mx = fmaxf(mx, shfl_xor(mx, 32));
+  const float mnew = fmaxf(m_c, mx);
+  const float alpha = fast_exp2(m_c - mnew);
+  m_c = mnew;
+  l_c *= alpha;
+#pragma unroll
+  for (int h = 0; h < NH; ++h)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int rl = 16 * h + 4 * lq + j;
+      const float p = rs + rl < re ? fast_exp2(s2[h][j] - mnew) : 0.f;
+      l_c += p;
+      if (lr < G) ps[rl * G + lr] = p;
+    }
+  if (lr < G && lq == 0) als[lr] = alpha;
+  fence_wave();
+  float al[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) al[g] = als[g];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[g][e] *= al[g];
+#pragma unroll
+  for (int u = 0; u < UV; ++u) {
+    float vf[8];
+    unpack8(vr[u], vf);
+    const int rl = u * RPI + rg;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float p = ps[rl * G + g];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+    }
+  }
+  fence_wave();  // the next tile rewrites ps / als
+}
+
+template <int D, int G, int U, bool FUSED, bool MF>
+__device__ __forceinline__ void decode_body(const DecodeArgs& a) {
+  constexpr int LPR = D / 8;       // lanes per row (V layout; K layout too without MF)
   constexpr int RPI = 64 / LPR;    // rows per load instruction
-  constexpr int T = RPI * U;       // rows per wave tile (<= 64)
+  constexpr int T = MF ? kMfmaTile : RPI * U;  // rows per wave tile (<= 64)
+  constexpr int UV = T / RPI;      // V load instructions per tile
+  constexpr int NK = D / 32;       // MFMA k-steps per 16 rows (MF only)
   static_assert(T <= 64, "one kept position per lane");
+  static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
   constexpr int KS = FUSED ? kMaxFusedSplit : 1;
+  constexpr int PS = MF ? kWaves : 1;
   __shared__ float red[kWaves][G][D + 2];
   __shared__ float wl_s[G][KS];    // fused: window logits of the split
   __shared__ int kp_s[KS];         // fused: kept positions of the split
+  __shared__ float p_s[PS][MF ? kMfmaTile : 1][G];  // MF: softmax weights, C -> V layout
+  __shared__ float alpha_s[PS][G];                  // MF: rescale factors of the tile
   extern __shared__ uint32_t bm_all[];  // fused: one skip bitmap per wave
 
   const int lane = threadIdx.x & 63;
@@ -219,11 +332,29 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   const uint16_t* vb = a.v + base;
   const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
 
-  uint4 qr[G];
+  uint4 qr[MF ? 1 : G];
+  if constexpr (!MF) {
 #pragma unroll
-  for (int g = 0; g < G; ++g)
-    qr[g] = *reinterpret_cast<const uint4*>(
-        a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
+    for (int g = 0; g < G; ++g)
+      qr[g] = *reinterpret_cast<const uint4*>(
+          a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
+  }
+  // MFMA operands: K in the A layout (lane l: row l%16, elements
+  // 8*(l/16) + 32*i .. +7 of k-step i), q^T in the B layout (lane l: query
+  // head l%16 of the group, same elements; zero for l%16 >= G).
+  const int lr = lane & 15, lq = lane >> 4;
+  const uint16_t* kmf = a.k + (base - c * 8) + 8 * lq;
+  bf16x8 qb[MF ? NK : 1];
+  if constexpr (MF) {
+#pragma unroll
+    for (int i = 0; i < NK; ++i) {
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (lr < G)
+        x = *reinterpret_cast<const uint4*>(
+            a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + lr) * D + 32 * i + 8 * lq);
+      qb[i] = __builtin_bit_cast(bf16x8, x);
+    }
+  }
 
   // Tiles never straddle the prompt/decode boundary: the split's prompt rows
   // [r0, pe) and decode rows [wst, r1) are each cut into tiles of T rows,
@@ -242,6 +373,7 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   // The wave holding window rank 0 (the first decode tile of the pair)
   // reports the plan's count and flags, as dsa_plan would.
   bool reporter = false;
+  int rep_flags = 0;
   if constexpr (FUSED) {
     // First window tile of this wave, if it has one.
     const int j0 = P + ((wave - P) % nwaves + nwaves) % nwaves;
@@ -263,19 +395,32 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
       }
       rank_window(a, pair, lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
     }
+    // The reporting wave settles the plan flags now, so the skip set is not
+    // live through the K/V loop.
+    if (reporter) {
+      rep_flags = rr.flags;
+      if (rr.t >= 0) {
+        rep_flags |= ss.flags;
+        const int kept = count_kept(ss, lane);
+        if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
+            kept != min(rr.t + 1, a.Natt))
+          rep_flags |= DSA_FLAG_COUNT;
+      }
+    }
     if (Wn > 0) __syncthreads();
   }
 
-  float qf[G][8];
+  float qf[MF ? 1 : G][8];
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    unpack8(qr[g], qf[g]);
+    if constexpr (!MF) unpack8(qr[g], qf[g]);
     m[g] = kNegBig;
     l[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   }
+  float m_c = kNegBig, l_c = 0.f;  // MF: running max / partial sum of head lr
 
   for (int j = wave; j < P + Wn; j += nwaves) {
     const bool dec = j >= P;
@@ -290,6 +435,11 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
       } else {
         if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
       }
+    }
+    if constexpr (MF) {
+      mfma_tile<D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, m_c, l_c,
+                             acc, &wl_s[0][0], &p_s[wave][0][0], &alpha_s[wave][0]);
+      continue;
     }
     uint4 kr[U], vr[U];
 #pragma unroll
@@ -362,25 +512,31 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   }
 
   if constexpr (FUSED) {
-    if (reporter) {
-      int flags = rr.flags;
-      if (rr.t >= 0) {
-        flags |= ss.flags;
-        const int kept = count_kept(ss, lane);
-        if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
-            kept != min(rr.t + 1, a.Natt))
-          flags |= DSA_FLAG_COUNT;
-      }
-      if (lane == 0) {
-        a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
-        a.plan_flags[pair] = flags;
-      }
+    if (reporter && lane == 0) {
+      a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
+      a.plan_flags[pair] = rep_flags;
     }
   }
 
+  if constexpr (MF) {
+    // Head g's running max sits in the lanes with lr == g; its sum is split
+    // over the four lanes lr + 16*q.  The V-layout accumulators of all row
+    // groups share that max, so they merge by plain addition.
+    float lt = l_c + shfl_xor(l_c, 16);
+    lt += shfl_xor(lt, 32);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      m[g] = __shfl(m_c, g, 64);
+      l[g] = __shfl(lt, g, 64);
+#pragma unroll
+      for (int off = LPR; off < 64; off <<= 1)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[g][e] += shfl_xor(acc[g][e], off);
+    }
+  }
   // Merge the row groups of the wave (lanes c, c + LPR, c + 2*LPR, ...).
 #pragma unroll
-  for (int off = LPR; off < 64; off <<= 1) {
+  for (int off = LPR; off < 64 && !MF; off <<= 1) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const float m2 = shfl_xor(m[g], off);
@@ -463,6 +619,20 @@ __global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
   }
 }
 
+template <int D, int G, int U, bool FUSED>
+__global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
+  decode_body<D, G, U, FUSED, false>(a);
+}
+
+// The grouped-head (MFMA) tile holds K and V of 32 rows plus G accumulator
+// sets; the occupancy floor keeps three waves per SIMD resident (two for
+// groups of eight, whose accumulators alone take 64 registers).
+template <int D, int G, bool FUSED>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : 3, 8)))
+void decode_mfma_kernel(DecodeArgs a) {
+  decode_body<D, G, 2, FUSED, true>(a);
+}
+
 // out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s over the splits of
 // (request b, query head g of KV head kvh), in base-2 exponents (the partial
 // maxima are kept in log2 units).  Called by one wave.
@@ -542,27 +712,42 @@ __global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
   }
 }
 
-template <int D, int G, int U, bool FUSED>
+template <int D, int G, int U, bool FUSED, bool MF>
 void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                   hipEvent_t t1) {
   const int grid = d.B * d.Hkv * d.S;
   const int block = 64 * d.NW;
   const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * d.NW * a.words) : 0u;
-  if (t0 || t1)
-    hipExtLaunchKernelGGL(decode_kernel<D, G, U, FUSED>, dim3(grid), dim3(block), lds, st, t0, t1,
-                          0, a);
-  else
-    decode_kernel<D, G, U, FUSED><<<grid, block, lds, st>>>(a);
+  if constexpr (MF) {
+    if (t0 || t1)
+      hipExtLaunchKernelGGL(decode_mfma_kernel<D, G, FUSED>, dim3(grid), dim3(block), lds, st, t0,
+                            t1, 0, a);
+    else
+      decode_mfma_kernel<D, G, FUSED><<<grid, block, lds, st>>>(a);
+  } else {
+    if (t0 || t1)
+      hipExtLaunchKernelGGL(decode_kernel<D, G, U, FUSED>, dim3(grid), dim3(block), lds, st, t0, t1,
+                            0, a);
+    else
+      decode_kernel<D, G, U, FUSED><<<grid, block, lds, st>>>(a);
+  }
 }
 
 template <int D, int G, bool FUSED>
 hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                      hipEvent_t t1) {
-  switch (d.U) {
-    case 8: launch_split<D, G, 8, FUSED>(d, a, st, t0, t1); break;
-    case 4: launch_split<D, G, 4, FUSED>(d, a, st, t0, t1); break;
-    default: launch_split<D, G, 2, FUSED>(d, a, st, t0, t1); break;
+  if constexpr (G >= 2) {
+    if (d.MF) {
+      launch_split<D, G, 2, FUSED, true>(d, a, st, t0, t1);
+      goto launched;
+    }
   }
+  switch (d.U) {
+    case 8: launch_split<D, G, 8, FUSED, false>(d, a, st, t0, t1); break;
+    case 4: launch_split<D, G, 4, FUSED, false>(d, a, st, t0, t1); break;
+    default: launch_split<D, G, 2, FUSED, false>(d, a, st, t0, t1); break;
+  }
+launched:
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || d.S <= 1) return e;
   if (FUSED) {

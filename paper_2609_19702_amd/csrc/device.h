@@ -26,6 +26,8 @@ __device__ __forceinline__ void unpack8(const uint4& r, float (&f)[8]) {
 // per step, so they should not push the small per-step buffers (queries,
 // selection state, plans) out of the caches.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 load_stream16(const void* p) {
   const u32x4 x = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
   return make_uint4(x.x, x.y, x.z, x.w);

@@ -24,6 +24,7 @@ struct Derived {
   int C;          // rows per split workgroup
   int S;          // splits per (request, KV head), upper bound
   int NW;         // waves per decode workgroup (1..kWaves)
+  bool MF;        // grouped query heads: q.K^T on MFMA
   size_t ws_bytes;
 };
 
@@ -31,6 +32,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 
 constexpr int kWaves = 4;          // waves per workgroup in every kernel
 constexpr int kBlock = 64 * kWaves;
+constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
 constexpr int kMaxFusedSplit = 256;  // rows per diagonal-mode split (fused step keeps them in LDS)
 constexpr int kMaxFusedWindow = 16384;  // N_r of the fused step (skip bitmap per wave in LDS)
 constexpr float kNegBig = -1.0e30f;  // "no score yet": finite, so exp2 of a difference is 0

@@ -99,7 +99,9 @@ def test_layouts_and_split_config(mode, shape, par):
     assert pl.bytes == B.plan_bytes(p, s) and pl.bytes >= pl.indices_offset + 4 * pairs * pl.cap
     assert sl.bytes == B.state_bytes(p, s) and sl.bytes >= sl.offsets_offset + 2 * pairs * sl.cap
     rows_max = p.prompt_len + (pl.cap if mode == 1 else L_dec)
-    block = (512 // s.head_dim) * li.kernel_variant
+    block = 32 if li.kernel_variant == 100 else (512 // s.head_dim) * li.kernel_variant
+    assert (li.kernel_variant == 100) == (s.num_q_heads > s.num_kv_heads)
+    assert 1 <= li.waves_per_group <= 4
     assert li.rows_per_split % block == 0
     assert li.rows_per_split * li.max_splits >= rows_max
     assert li.rows_per_split * (li.max_splits - 1) < max(rows_max, 1)
