@@ -89,7 +89,15 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   const int block_rows = d->MF ? kMfmaTile : rows_per_instr * d->U;
   const int64_t rows_max = d->Lp + (diag ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
-  const int64_t split_bytes = env_int("DSA_TUNE_SPLIT_KB", 48) * int64_t(1024);
+  // Measured on MI355X: diagonal splits of ~48 KB; dense splits of ~24 KB
+  // for d = 64 (long ragged rows balance better), ~48 KB for d = 128 and
+  // ~96 KB for the grouped-head tile (fewer partials to merge).
+  // The grouped-head tile also prefers ~96 KB diagonal splits.
+  const int dense_kb = d->MF ? 96 : (d->D == 64 ? 24 : 48);
+  const int diag_kb = d->MF ? 96 : 48;
+  const int64_t split_bytes =
+      (diag ? env_int("DSA_TUNE_SPLIT_KB", diag_kb) : env_int("DSA_TUNE_SPLIT_KB_DENSE", dense_kb)) *
+      int64_t(1024);
   int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
   if (diag) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);

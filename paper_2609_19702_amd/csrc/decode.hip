@@ -642,6 +642,7 @@ __device__ __forceinline__ void combine_one(const DecodeArgs& a, int lane, int b
   const int pair = b * a.Hkv + kvh;
   const float* pp = a.part + (static_cast<size_t>(pair) * a.S * G + g) * (D + 2);
   const size_t sstride = static_cast<size_t>(G) * (D + 2);
+  // Maxima and sums: one split per lane.
   float M = kNegBig;
   for (int s = lane; s < nsplit; s += 64) M = fmaxf(M, pp[s * sstride + D]);
   M = wave_max(M);
@@ -649,11 +650,27 @@ __device__ __forceinline__ void combine_one(const DecodeArgs& a, int lane, int b
   for (int s = lane; s < nsplit; s += 64)
     L += pp[s * sstride + D + 1] * fast_exp2(pp[s * sstride + D] - M);
   L = wave_sum(L);
+  // Weighted rows: lanes over columns, eight splits' loads in flight.
   float A0 = 0.f, A1 = 0.f;
-  for (int s = 0; s < nsplit; ++s) {
-    const float sw = fast_exp2(pp[s * sstride + D] - M);
-    A0 += pp[s * sstride + lane] * sw;
-    if constexpr (D == 128) A1 += pp[s * sstride + lane + 64] * sw;
+  for (int s0 = 0; s0 < nsplit; s0 += 64) {
+    const int sl = s0 + lane;
+    const float w = sl < nsplit ? fast_exp2(pp[sl * sstride + D] - M) : 0.f;
+    const int n = min(64, nsplit - s0);
+    for (int j0 = 0; j0 < n; j0 += 8) {
+      float x0[8], x1[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int sj = s0 + min(j0 + j, n - 1);
+        x0[j] = pp[sj * sstride + lane];
+        if constexpr (D == 128) x1[j] = pp[sj * sstride + lane + 64];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float sw = j0 + j < n ? __shfl(w, j0 + j, 64) : 0.f;
+        A0 = fmaf(x0[j], sw, A0);
+        if constexpr (D == 128) A1 = fmaf(x1[j], sw, A1);
+      }
+    }
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
   float* o = a.out + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D;
@@ -675,21 +692,23 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
   combine_one<D>(a, lane, b, h / G, h % G, G, nsplit);
 }
 
-// Fused step, several splits: one wave per (request, KV head) merges the
-// splits of every query head of the group, then runs the phase-2 selection
-// on the window logits and the plan the split workgroups wrote.
+// Fused step, several splits: one workgroup per (request, KV head).  Its
+// waves merge the splits of the group's query heads (head g on wave g mod 4)
+// while the last wave also runs the phase-2 selection on the window logits
+// and the plan the split workgroups wrote (the selection does not depend on
+// the merged outputs).
 template <int D, int G>
 __global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
-  const int pair = blockIdx.x * kWaves + (threadIdx.x >> 6);
-  if (pair >= a.B * a.Hkv) return;
+  const int wave = threadIdx.x >> 6;
+  const int pair = blockIdx.x;
   const int b = pair / a.Hkv;
   const int kvh = pair % a.Hkv;
   const RowRange rr = row_range<true>(a, b, pair);
   const int nsplit = (rr.n + a.C - 1) / a.C;
   if (nsplit <= 1) return;
-#pragma unroll
-  for (int g = 0; g < G; ++g) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
+  for (int g = wave; g < G; g += kWaves) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
+  if (wave != kWaves - 1) return;
   const int t = rr.t;
   if (t < a.Natt - 1 || t > a.Nr - 2) return;
   const int k = t - (a.Natt - 1);
@@ -751,8 +770,7 @@ launched:
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || d.S <= 1) return e;
   if (FUSED) {
-    const int cgrid = (d.B * d.Hkv + kWaves - 1) / kWaves;
-    combine_select_kernel<D, G><<<cgrid, kBlock, 0, st>>>(a);
+    combine_select_kernel<D, G><<<d.B * d.Hkv, kBlock, 0, st>>>(a);
   } else {
     const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
     combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
