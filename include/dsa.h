@@ -108,20 +108,30 @@ typedef struct dsa_shape {
 
 /*
  * Where row r of KV head h of request b lives in the K and V arrays (both
- * arrays share one layout).  Rows 0 .. L_p-1 are the prompt; decode position
- * j is row L_p + j.  Element offset of the row's first element:
+ * arrays share one layout).  Rows 0 .. L_p-1 are the prompt.  Element offset
+ * of a row's first element:
  *     base(b) + h * stride_head + r * stride_row
  * with base(b) = d_row_base[b] when d_row_base is non-NULL (a device array of
  * B int64 values, e.g. for ragged packing), else b * stride_batch.
+ * Decode position j is row L_p + j (ring_rows = 0, a linear cache), or row
+ * L_p + (j mod ring_rows) when ring_rows > 0: a ring of ring_rows slots in
+ * which the KV of position j overwrites that of position j - ring_rows.  In
+ * diagonal mode this is the physical form of Algorithm 1's eviction (phase 3
+ * drops K[t - N_r]; section 4, "Cost analysis": the footprint is bounded by
+ * N_r + L_p), and needs ring_rows >= N_r; dense mode needs every decode row,
+ * so a ring must hold ring_rows >= H*W there.
  * A row holds head_dim contiguous bf16 values.  The K/V base pointers and
  * every base(b), stride_head and stride_row must be multiples of 8 elements
- * (16 bytes).  The caller guarantees every row up to L_p + t_b exists.
+ * (16 bytes).  The caller guarantees every row the step reads exists and
+ * holds the KV of the position it stands for (linear: rows up to L_p + t_b;
+ * ring: the slots of positions t_b - N_r + 1 .. t_b).
  */
 typedef struct dsa_kv_layout {
   const int64_t* d_row_base;
   int64_t stride_batch;
   int64_t stride_head;
   int64_t stride_row;
+  int64_t ring_rows;
 } dsa_kv_layout;
 
 /* Byte offsets of the arrays inside a plan buffer (all int32):

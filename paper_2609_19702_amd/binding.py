@@ -54,7 +54,8 @@ class Shape(C.Structure):
 
 class KVLayout(C.Structure):
     _fields_ = [("d_row_base", C.c_void_p), ("stride_batch", C.c_int64),
-                ("stride_head", C.c_int64), ("stride_row", C.c_int64)]
+                ("stride_head", C.c_int64), ("stride_row", C.c_int64),
+                ("ring_rows", C.c_int64)]
 
 
 class PlanLayout(C.Structure):
@@ -217,13 +218,15 @@ def plan(p, s, decode_pos, state, plan_buf, stream=None):
                           plan_buf.numel() * plan_buf.element_size(), _stream(stream)), "dsa_plan")
 
 
-def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None) -> KVLayout:
+def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None,
+              ring_rows: int = 0) -> KVLayout:
     """Layout of a ``[B, Hkv, rows, d]`` cache (any strides with unit stride
-    along d); ``row_base`` optionally gives per-request base offsets."""
+    along d); ``row_base`` optionally gives per-request base offsets;
+    ``ring_rows > 0`` stores decode position j at row ``L_p + j % ring_rows``."""
     sb, sh, sr, sd = k.stride()
     if sd != 1:
         raise ValueError("head_dim must be contiguous")
-    return KVLayout(_ptr(row_base), sb, sh, sr)
+    return KVLayout(_ptr(row_base), sb, sh, sr, int(ring_rows))
 
 
 def decode_attention(p, s, q, k, v, layout: KVLayout, decode_pos, plan_buf, sm_scale, out,

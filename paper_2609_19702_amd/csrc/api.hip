@@ -308,6 +308,10 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   if (kv->stride_row < d.D || kv->stride_head < 0 || kv->stride_batch < 0)
     return DSA_ERR_INVALID_ARG;
   if ((kv->stride_row | kv->stride_head | kv->stride_batch) & 7) return DSA_ERR_INVALID_ARG;
+  if (kv->ring_rows < 0 || kv->ring_rows > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
+  if (kv->ring_rows > 0 &&
+      kv->ring_rows < (d.mode == DSA_MODE_DIAGONAL ? int64_t(d.Nr) : int64_t(d.Ldec)))
+    return DSA_ERR_INVALID_ARG;  // the ring must hold every row the step can read
   if ((reinterpret_cast<uintptr_t>(d_k) | reinterpret_cast<uintptr_t>(d_v) |
        reinterpret_cast<uintptr_t>(d_q)) & 15)
     return DSA_ERR_INVALID_ARG;
@@ -338,6 +342,8 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   a.plan_cap = d.plan_cap;
   a.C = d.C;
   a.S = d.S;
+  // A ring of at least L_dec slots maps every position to itself.
+  a.ring = kv->ring_rows >= d.Ldec ? 0 : static_cast<int>(kv->ring_rows);
   a.Nr = d.Nr;
   a.Natt = d.Natt;
   a.state_cap = d.state_cap;

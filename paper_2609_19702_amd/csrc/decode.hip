@@ -22,6 +22,8 @@
 //     kept positions of a window tile are held one per lane and handed to
 //     the row groups with ds_bpermute, prompt tiles need none;
 //   - K/V rows are loaded with the non-temporal hint (streamed once);
+//   - with a ring layout a kept decode position j is read from slot
+//     j mod ring (the ring holds the live window; evicted rows are gone);
 //   - a workgroup has as many waves (1..4) as its split has tiles, so no wave
 //     sits idle holding registers;
 //   - q.k partial sums are reduced inside the row's lane group with DPP row
@@ -435,6 +437,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       } else {
         if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
       }
+      if (a.ring) pos_l %= a.ring;  // decode position -> ring slot
     }
     if constexpr (MF) {
       mfma_tile<D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, m_c, l_c,

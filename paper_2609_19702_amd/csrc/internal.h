@@ -62,6 +62,7 @@ struct DecodeArgs {
   float* wlog;           // window logits or nullptr
   float* part;           // split partials (S > 1)
   int B, Hq, Hkv, Lp, Ldec, mode, plan_cap, C, S;
+  int ring;              // decode rows in a ring of this many slots (0: linear)
   // fused step only: selection state (in/out) and plan (out)
   int32_t* st_count;
   int32_t* st_flags;

@@ -151,7 +151,7 @@ def test_token_major_layout_with_row_base():
     packed_k = torch.cat([kv.k[b, :, :rows[b]].transpose(0, 1).reshape(-1) for b in range(s.batch)])
     packed_v = torch.cat([kv.v[b, :, :rows[b]].transpose(0, 1).reshape(-1) for b in range(s.batch)])
     base = torch.tensor(np.cumsum([0] + [r * Hkv * d for r in rows[:-1]]), dtype=torch.int64, device=DEV)
-    lay = B.KVLayout(base.data_ptr(), 0, d, Hkv * d)
+    lay = B.KVLayout(base.data_ptr(), 0, d, Hkv * d, 0)
     bufs = B.alloc_buffers(p, s, DEV)
     B.plan(p, s, pos, st_buf, bufs.plan)
     B.decode_attention(p, s, q, packed_k, packed_v, lay, pos, bufs.plan, 1 / math.sqrt(d),
@@ -174,7 +174,7 @@ def test_decode_argument_errors():
         B.decode_attention(pdg, s, q, kv.k, kv.v, lay, pos, None, 0.125, bufs.out, None,
                            bufs.workspace)
     assert e.value.status == B.ERR_INVALID_ARG
-    bad = B.KVLayout(None, lay.stride_batch, lay.stride_head, 60)
+    bad = B.KVLayout(None, lay.stride_batch, lay.stride_head, 60, 0)
     with pytest.raises(B.DSAError) as e:
         B.decode_attention(p, s, q, kv.k, kv.v, bad, pos, None, 0.125, bufs.out, None, bufs.workspace)
     assert e.value.status == B.ERR_INVALID_ARG
