@@ -14,6 +14,10 @@
  *     relative offset d = t - j, which never changes, so the per-step "shift"
  *     of the algorithm costs nothing;
  *   - each step attends exactly min(t + 1, N_att) decode rows;
+ *   - the variants of section 5.1 keep the first S decode tokens as
+ *     attention sinks ("Diagonal+Sink4": Algorithm 1 on the later tokens;
+ *     StreamingLLM: the sinks plus a recent window; S = 0 is the plain
+ *     sliding window);
  *   - a dense mode (all decode rows 0 .. t) is the baseline the paper
  *     compares against in its evaluation (section 5).
  *
@@ -54,7 +58,7 @@ extern "C" {
 
 #define DSA_API __attribute__((visibility("default")))
 
-#define DSA_ABI_VERSION 1
+#define DSA_ABI_VERSION 2
 
 /* ---- status codes -------------------------------------------------------- */
 typedef int32_t dsa_status;
@@ -67,6 +71,7 @@ typedef int32_t dsa_status;
 /* ---- modes ----------------------------------------------------------------- */
 #define DSA_MODE_DENSE    0 /* attend prompt + decode rows 0 .. t            */
 #define DSA_MODE_DIAGONAL 1 /* attend prompt + the rows Algorithm 1 keeps     */
+#define DSA_MODE_WINDOW   2 /* attend prompt + sinks + the most recent rows   */
 
 /* ---- per-(request, KV head) flag bits (plan and state buffers) ------------ */
 #define DSA_FLAG_INACTIVE      1  /* decode position < 0: request slot unused   */
@@ -76,12 +81,22 @@ typedef int32_t dsa_status;
 #define DSA_FLAG_COUNT         16 /* kept count differs from min(t+1, N_att)    */
 
 /*
- * Method parameters (Algorithm 1 inputs, section 4).
+ * Method parameters (Algorithm 1 inputs, section 4; sinks, section 5.1).
  *   prompt_len  L_p >= 0, prompt rows always attended
  *   grid_h/w    visual token grid, >= 1; L_dec = grid_h * grid_w decode steps
- *   window      N_r, recent window, 1 <= N_r <= 65535
- *   n_att       N_att, decode rows attended per step, 1 <= N_att <= N_r
- *   mode        DSA_MODE_DENSE or DSA_MODE_DIAGONAL
+ *   window      N_r, recent window, 1 <= N_r <= 65535 (checked in every
+ *               mode, used by DSA_MODE_DIAGONAL only)
+ *   n_att       N_att, decode rows attended per step, including the sinks;
+ *               1 <= N_att, and N_att <= N_r in DSA_MODE_DIAGONAL
+ *   mode        DSA_MODE_DENSE, DSA_MODE_DIAGONAL or DSA_MODE_WINDOW
+ *   sinks       S, 0 <= S < N_att: decode positions 0 .. S-1 are always
+ *               attended once decoded.  DSA_MODE_DIAGONAL runs Algorithm 1
+ *               on the positions after them as if position S were step 0
+ *               (window N_r, N_att - S rows to attend: "Diagonal+Sink4" is
+ *               S = 4); DSA_MODE_WINDOW attends the sinks plus the
+ *               N_att - S most recent positions (StreamingLLM is S = 4, the
+ *               sliding window S = 0).  Ignored in dense mode.
+ * In every sparse mode a step attends min(t + 1, N_att) decode rows.
  */
 typedef struct dsa_params {
   int32_t prompt_len;
@@ -90,6 +105,7 @@ typedef struct dsa_params {
   int32_t window;
   int32_t n_att;
   int32_t mode;
+  int32_t sinks;
 } dsa_params;
 
 /*
@@ -113,18 +129,20 @@ typedef struct dsa_shape {
  *     base(b) + h * stride_head + r * stride_row
  * with base(b) = d_row_base[b] when d_row_base is non-NULL (a device array of
  * B int64 values, e.g. for ragged packing), else b * stride_batch.
- * Decode position j is row L_p + j (ring_rows = 0, a linear cache), or row
- * L_p + (j mod ring_rows) when ring_rows > 0: a ring of ring_rows slots in
- * which the KV of position j overwrites that of position j - ring_rows.  In
+ * Decode position j is row L_p + j (ring_rows = 0, a linear cache), or,
+ * when ring_rows = R > 0, a ring: the S sink positions keep rows
+ * L_p .. L_p + S - 1 (S = 0 in dense mode) and position j >= S lives in row
+ * L_p + S + ((j - S) mod (R - S)), overwriting position j - (R - S).  In
  * diagonal mode this is the physical form of Algorithm 1's eviction (phase 3
  * drops K[t - N_r]; section 4, "Cost analysis": the footprint is bounded by
- * N_r + L_p), and needs ring_rows >= N_r; dense mode needs every decode row,
- * so a ring must hold ring_rows >= H*W there.
+ * N_r + L_p) and needs R >= S + N_r; window mode needs R >= N_att; dense
+ * mode reads every decode row, so a ring must hold R >= H*W there.  A ring
+ * of R >= H*W rows is the linear cache.
  * A row holds head_dim contiguous bf16 values.  The K/V base pointers and
  * every base(b), stride_head and stride_row must be multiples of 8 elements
  * (16 bytes).  The caller guarantees every row the step reads exists and
  * holds the KV of the position it stands for (linear: rows up to L_p + t_b;
- * ring: the slots of positions t_b - N_r + 1 .. t_b).
+ * ring: the sinks and the slots of the positions the step can keep).
  */
 typedef struct dsa_kv_layout {
   const int64_t* d_row_base;
@@ -138,7 +156,7 @@ typedef struct dsa_kv_layout {
  *   count  [B*Hkv]           kept decode rows of (b, h), index b*Hkv + h
  *   flags  [B*Hkv]           DSA_FLAG_* bits
  *   indices[B*Hkv][cap]      kept decode positions of (b, h), ascending
- * cap = min(N_att, L_dec) in diagonal mode and 0 in dense mode.           */
+ * cap = min(N_att, L_dec) in the sparse modes and 0 in dense mode.       */
 typedef struct dsa_plan_layout {
   size_t count_offset;
   size_t flags_offset;
@@ -152,7 +170,9 @@ typedef struct dsa_plan_layout {
  *   flags   int32  [B*Hkv]        DSA_FLAG_* bits set by dsa_select
  *   offsets uint16 [B*Hkv][cap]   skip entries as offsets d = t - j, in the
  *                                 order Algorithm 1 appends them
- * cap = N_r - N_att (the largest skip list of Algorithm 1).               */
+ * cap = N_r - (N_att - S) in diagonal mode (the largest skip list of
+ * Algorithm 1 over the positions after the S sinks), 0 in the other modes
+ * (nothing is selected; the state buffer may then be NULL everywhere).    */
 typedef struct dsa_state_layout {
   size_t count_offset;
   size_t flags_offset;
@@ -184,14 +204,17 @@ DSA_API const char* dsa_status_str(dsa_status status);
  * Fill *out from a target sparsity (section 5.1: sparsity = 1 - N_att/L_dec)
  * and the window rule of the "Parameter selection" paragraph of section 4.
  *   window = 0 selects the paper's default N_r = L_dec / 2 (at least 1);
- *   n_att = clamp(floor((1000 - sparsity_permille) * L_dec / 1000 + 1/2),
- *                 1, N_r), computed in integers.
+ *   n_att = floor((1000 - sparsity_permille) * L_dec / 1000 + 1/2),
+ *           computed in integers, then raised to at least sinks + 1 and, in
+ *           dense and diagonal mode, lowered to at most N_r (window mode
+ *           keeps it up to L_dec: its recent window is not bounded by N_r).
  * Errors: DSA_ERR_INVALID_ARG for out == NULL, sparsity outside [0, 1000],
- * negative prompt_len, grid < 1, window outside [0, 65535] or a bad mode.
+ * negative prompt_len, grid < 1, window outside [0, 65535], a bad mode,
+ * sinks < 0, or sinks >= N_r in diagonal mode.
  */
 DSA_API dsa_status dsa_params_from_sparsity(int32_t prompt_len, int32_t grid_h, int32_t grid_w,
                                             int32_t window, int32_t sparsity_permille,
-                                            int32_t mode, dsa_params* out);
+                                            int32_t mode, int32_t sinks, dsa_params* out);
 
 /* Validate a parameter/shape pair as every device call does.  Returns
  * DSA_OK, DSA_ERR_INVALID_ARG or DSA_ERR_UNSUPPORTED. */
@@ -231,13 +254,16 @@ DSA_API dsa_status dsa_state_reset(const dsa_params* p, const dsa_shape* s, void
  *                 (its K/V row L_p + t_b is already written); t_b < 0 marks
  *                 an unused slot (count 0, output zeros).
  *   d_state       selection state; the step uses the first
- *                 clamp(t_b - N_att + 1, 0, N_r - N_att) entries of each list
+ *                 clamp(t_b - N_att + 1, 0, state cap) entries of each list
  *                 (the entries appended at steps < t_b), so replaying a step
- *                 is exact.  Ignored (may be NULL) in dense mode.
+ *                 is exact.  Ignored (may be NULL) when the state cap is 0
+ *                 (dense and window mode, or N_att - S = N_r).
  *   d_plan        output, plan_bytes >= dsa_plan_bytes().  For each (b, h):
- *                 count = kept rows (diagonal: min(t_b+1, N_att)), flags,
- *                 and in diagonal mode the kept positions t_b - d for offsets
- *                 d in [0, min(t_b, N_r-1)] not in the skip list, ascending.
+ *                 count = kept rows (sparse modes: min(t_b+1, N_att)), flags,
+ *                 and in the sparse modes the kept positions, ascending: the
+ *                 sinks 0 .. min(S, t_b+1)-1, then t_b - d for the offsets
+ *                 d in [0, min(t_b - S, W - 1)] not in the skip list, with
+ *                 W = N_r (diagonal) or N_att - S (window).
  * Errors: INVALID_ARG (NULL pointers, bad params), UNSUPPORTED, WORKSPACE
  * (plan_bytes too small), HIP.
  */
@@ -255,13 +281,14 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
  *   d_q              bf16 [B][Hq][d]
  *   d_k, d_v         bf16 caches in the dsa_kv_layout layout
  *   d_decode_pos     int32 [B] as for dsa_plan
- *   d_plan           plan of the same step (diagonal mode); may be NULL in
+ *   d_plan           plan of the same step (sparse modes); may be NULL in
  *                    dense mode
  *   sm_scale         softmax scale, normally 1/sqrt(d)
  *   d_out            fp32 [B][Hq][d]; zeros for unused slots
  *   d_window_logits  NULL, or fp32 [B][Hq][cap]: sm_scale * q . k of every
- *                    kept decode row in plan order (diagonal mode; entries
- *                    past count are not written).  dsa_select reads them.
+ *                    kept decode row in plan order, sinks included (sparse
+ *                    modes; entries past count are not written).  dsa_select
+ *                    reads them.
  *   d_ws, ws_bytes   workspace of at least dsa_workspace_bytes() bytes
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
  */
@@ -301,12 +328,14 @@ DSA_API dsa_status dsa_decode_attention_timed(const dsa_params* p, const dsa_sha
  * argmin and appends the skip entry, otherwise a second kernel merges the
  * splits and selects.  In dense mode it is dsa_decode_attention and d_state,
  * d_plan and d_window_logits are not used.
- *   d_state          selection state, in/out (diagonal mode)
+ *   d_state          selection state, in/out; may be NULL when the state
+ *                    cap is 0 (window mode, or N_att - S = N_r)
  *   d_plan           plan of this step, out; plan_bytes >= dsa_plan_bytes()
- *   d_window_logits  fp32 [B][Hq][cap], out; required in diagonal mode
+ *   d_window_logits  fp32 [B][Hq][cap], out; required when the state cap is
+ *                    not 0, else optional
  *   other arguments  as for dsa_decode_attention
  * Errors: as dsa_decode_attention; UNSUPPORTED for N_r > 16384 in diagonal
- * mode (use the three separate calls there).
+ * mode with a non-zero state cap (use the three separate calls there).
  */
 DSA_API dsa_status dsa_decode_step(const dsa_params* p, const dsa_shape* s, const void* d_q,
                                    const void* d_k, const void* d_v, const dsa_kv_layout* kv,
@@ -327,15 +356,17 @@ DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s
 
 /*
  * Phase-2 selection of Algorithm 1: for every request with
- * N_att - 1 <= t_b <= N_r - 2 and every KV head h, compute
+ * N_att - 1 <= t_b <= N_r + S - 2 and every KV head h, compute
  *   w_q = softmax(window logits of query head q)   over the kept window
+ *                                                  (the sinks excluded)
  *   sigma_j = sum of w_q[j] over the query heads q that read KV head h
  *   j* = argmin_j sigma_j (first, i.e. oldest, on ties)
  * and store offset t_b - idx[j*] as skip entry number k = t_b - N_att + 1
  * (count becomes k + 1).  At group size 1 the argmin is taken on the logits,
- * which orders exactly as the softmax.  Requests outside that step range, and
- * dense mode, are left untouched.  A state with fewer than k entries is left
- * unchanged and flagged DSA_FLAG_STATE_BEHIND.
+ * which orders exactly as the softmax.  Requests outside that step range,
+ * and the modes without a selection state, are left untouched.  A state
+ * with fewer than k entries is left unchanged and flagged
+ * DSA_FLAG_STATE_BEHIND.
  *   d_plan, d_window_logits  from dsa_plan / dsa_decode_attention of this step
  *   d_state                  in/out
  * Errors: INVALID_ARG, UNSUPPORTED, HIP.

@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_PKG, "libdsa.so")
 
 MODE_DENSE = 0
 MODE_DIAGONAL = 1
+MODE_WINDOW = 2
 
 FLAG_INACTIVE = 1
 FLAG_POS_CLAMPED = 2
@@ -40,11 +41,12 @@ class DSAError(RuntimeError):
 
 class Params(C.Structure):
     _fields_ = [("prompt_len", C.c_int32), ("grid_h", C.c_int32), ("grid_w", C.c_int32),
-                ("window", C.c_int32), ("n_att", C.c_int32), ("mode", C.c_int32)]
+                ("window", C.c_int32), ("n_att", C.c_int32), ("mode", C.c_int32),
+                ("sinks", C.c_int32)]
 
     def __repr__(self):
         return (f"Params(prompt_len={self.prompt_len}, grid={self.grid_h}x{self.grid_w}, "
-                f"window={self.window}, n_att={self.n_att}, mode={self.mode})")
+                f"window={self.window}, n_att={self.n_att}, mode={self.mode}, sinks={self.sinks})")
 
 
 class Shape(C.Structure):
@@ -80,7 +82,7 @@ _VP = C.c_void_p
 SIGNATURES = {
     "dsa_abi_version": (C.c_int32, []),
     "dsa_status_str": (C.c_char_p, [C.c_int32]),
-    "dsa_params_from_sparsity": (C.c_int32, [C.c_int32] * 6 + [_P]),
+    "dsa_params_from_sparsity": (C.c_int32, [C.c_int32] * 7 + [_P]),
     "dsa_validate": (C.c_int32, [_P, _S]),
     "dsa_get_state_layout": (C.c_int32, [_P, _S, C.POINTER(StateLayout)]),
     "dsa_get_plan_layout": (C.c_int32, [_P, _S, C.POINTER(PlanLayout)]),
@@ -151,15 +153,15 @@ def abi_version() -> int:
     return lib().dsa_abi_version()
 
 
-def make_params(prompt_len, grid_h, grid_w, window, n_att, mode=MODE_DIAGONAL) -> Params:
-    return Params(prompt_len, grid_h, grid_w, window, n_att, mode)
+def make_params(prompt_len, grid_h, grid_w, window, n_att, mode=MODE_DIAGONAL, sinks=0) -> Params:
+    return Params(prompt_len, grid_h, grid_w, window, n_att, mode, sinks)
 
 
 def params_from_sparsity(prompt_len, grid_h, grid_w, window, sparsity_permille,
-                         mode=MODE_DIAGONAL) -> Params:
+                         mode=MODE_DIAGONAL, sinks=0) -> Params:
     p = Params()
     _check(lib().dsa_params_from_sparsity(prompt_len, grid_h, grid_w, window,
-                                          sparsity_permille, mode, C.byref(p)),
+                                          sparsity_permille, mode, sinks, C.byref(p)),
            "dsa_params_from_sparsity")
     return p
 
@@ -222,7 +224,8 @@ def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None,
               ring_rows: int = 0) -> KVLayout:
     """Layout of a ``[B, Hkv, rows, d]`` cache (any strides with unit stride
     along d); ``row_base`` optionally gives per-request base offsets;
-    ``ring_rows > 0`` stores decode position j at row ``L_p + j % ring_rows``."""
+    ``ring_rows = R > 0`` stores decode position ``j`` at row ``L_p + j``
+    for the ``S`` sinks and at ``L_p + S + (j - S) % (R - S)`` after them."""
     sb, sh, sr, sd = k.stride()
     if sd != 1:
         raise ValueError("head_dim must be contiguous")

@@ -23,9 +23,14 @@ int env_int(const char* name, int fallback) {
 dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   if (!p || !s || !d) return DSA_ERR_INVALID_ARG;
   if (p->prompt_len < 0 || p->grid_h < 1 || p->grid_w < 1) return DSA_ERR_INVALID_ARG;
-  if (p->mode != DSA_MODE_DENSE && p->mode != DSA_MODE_DIAGONAL) return DSA_ERR_INVALID_ARG;
+  if (p->mode != DSA_MODE_DENSE && p->mode != DSA_MODE_DIAGONAL && p->mode != DSA_MODE_WINDOW)
+    return DSA_ERR_INVALID_ARG;
   if (p->window < 1 || p->window > 65535) return DSA_ERR_INVALID_ARG;
-  if (p->n_att < 1 || p->n_att > p->window) return DSA_ERR_INVALID_ARG;
+  // Window mode's recent window is N_att - S, not bounded by N_r.
+  if (p->n_att < 1 || p->n_att > (p->mode == DSA_MODE_WINDOW ? (1 << 24) : p->window))
+    return DSA_ERR_INVALID_ARG;
+  if (p->sinks < 0 || (p->mode != DSA_MODE_DENSE && p->sinks >= p->n_att))
+    return DSA_ERR_INVALID_ARG;
   const int64_t ldec = static_cast<int64_t>(p->grid_h) * p->grid_w;
   if (ldec > (1 << 24) || p->prompt_len > (1 << 24)) return DSA_ERR_INVALID_ARG;
   if (s->batch < 1 || s->num_q_heads < 1 || s->num_kv_heads < 1) return DSA_ERR_INVALID_ARG;
@@ -44,12 +49,14 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->D = s->head_dim;
   d->Lp = p->prompt_len;
   d->Ldec = static_cast<int>(ldec);
-  d->Nr = p->window;
   d->Natt = p->n_att;
   d->mode = p->mode;
-  const bool diag = p->mode == DSA_MODE_DIAGONAL;
-  d->plan_cap = diag ? static_cast<int>(std::min<int64_t>(p->n_att, ldec)) : 0;
-  d->state_cap = p->window - p->n_att;
+  const bool sparse = p->mode != DSA_MODE_DENSE;  // a plan of kept rows (diagonal or window mode)
+  d->Ns = sparse ? p->sinks : 0;
+  d->Nr = p->mode == DSA_MODE_WINDOW ? p->n_att - p->sinks : p->window;
+  d->plan_cap = sparse ? static_cast<int>(std::min<int64_t>(p->n_att, ldec)) : 0;
+  d->state_cap = p->mode == DSA_MODE_DIAGONAL ? p->window - (p->n_att - p->sinks) : 0;
+  d->words = d->state_cap > 0 ? (d->Nr + 31) / 32 : 0;
   if (pairs * std::max(d->plan_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
   if (pairs * std::max(d->state_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
 
@@ -87,19 +94,19 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   // DSA_TUNE_VALU_GQA=1 asks for the vector-ALU tile.
   d->MF = G >= 2 && env_int("DSA_TUNE_VALU_GQA", 0) != 1;
   const int block_rows = d->MF ? kMfmaTile : rows_per_instr * d->U;
-  const int64_t rows_max = d->Lp + (diag ? d->plan_cap : ldec);
+  const int64_t rows_max = d->Lp + (sparse ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
-  // Measured on MI355X: diagonal splits of ~48 KB; dense splits of ~24 KB
+  // Measured on MI355X: sparse-mode splits of ~48 KB; dense splits of ~24 KB
   // for d = 64 (long ragged rows balance better), ~48 KB for d = 128 and
   // ~96 KB for the grouped-head tile (fewer partials to merge).
-  // The grouped-head tile also prefers ~96 KB diagonal splits.
+  // The grouped-head tile also prefers ~96 KB sparse-mode splits.
   const int dense_kb = d->MF ? 96 : (d->D == 64 ? 24 : 48);
   const int diag_kb = d->MF ? 96 : 48;
   const int64_t split_bytes =
-      (diag ? env_int("DSA_TUNE_SPLIT_KB", diag_kb) : env_int("DSA_TUNE_SPLIT_KB_DENSE", dense_kb)) *
+      (sparse ? env_int("DSA_TUNE_SPLIT_KB", diag_kb) : env_int("DSA_TUNE_SPLIT_KB_DENSE", dense_kb)) *
       int64_t(1024);
   int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
-  if (diag) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
+  if (sparse) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
   const int64_t min_wgs = env_int("DSA_TUNE_MIN_WGS", 512);
   if (pairs * S < min_wgs) {
@@ -150,24 +157,28 @@ DSA_API const char* dsa_status_str(dsa_status st) {
 
 DSA_API dsa_status dsa_params_from_sparsity(int32_t prompt_len, int32_t grid_h, int32_t grid_w,
                                             int32_t window, int32_t sparsity_permille,
-                                            int32_t mode, dsa_params* out) {
+                                            int32_t mode, int32_t sinks, dsa_params* out) {
   if (!out || sparsity_permille < 0 || sparsity_permille > 1000) return DSA_ERR_INVALID_ARG;
   if (prompt_len < 0 || grid_h < 1 || grid_w < 1 || window < 0 || window > 65535)
     return DSA_ERR_INVALID_ARG;
-  if (mode != DSA_MODE_DENSE && mode != DSA_MODE_DIAGONAL) return DSA_ERR_INVALID_ARG;
+  if (mode != DSA_MODE_DENSE && mode != DSA_MODE_DIAGONAL && mode != DSA_MODE_WINDOW)
+    return DSA_ERR_INVALID_ARG;
   const int64_t ldec = static_cast<int64_t>(grid_h) * grid_w;
-  if (ldec > (1 << 24)) return DSA_ERR_INVALID_ARG;
+  if (ldec > (1 << 24) || sinks < 0) return DSA_ERR_INVALID_ARG;
   int64_t nr = window;
   if (nr == 0) nr = std::max<int64_t>(1, std::min<int64_t>(ldec / 2, 65535));
   // round((1 - s) * L_dec) with ties up: floor((2 * (1000 - s) * L_dec + 1000) / 2000)
   int64_t natt = (2 * (1000 - int64_t(sparsity_permille)) * ldec + 1000) / 2000;
-  natt = std::min(nr, std::max<int64_t>(1, natt));
+  natt = std::max<int64_t>(natt, int64_t(sinks) + 1);
+  if (mode != DSA_MODE_WINDOW) natt = std::min(nr, natt);
+  if (mode == DSA_MODE_DIAGONAL && sinks >= natt) return DSA_ERR_INVALID_ARG;
   out->prompt_len = prompt_len;
   out->grid_h = grid_h;
   out->grid_w = grid_w;
   out->window = static_cast<int32_t>(nr);
   out->n_att = static_cast<int32_t>(natt);
   out->mode = mode;
+  out->sinks = sinks;
   return DSA_OK;
 }
 
@@ -261,14 +272,15 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
   dsa_status st = dsa::derive(p, s, &d);
   if (st != DSA_OK) return st;
   if (!d_decode_pos || !d_plan) return DSA_ERR_INVALID_ARG;
-  if (d.mode == DSA_MODE_DIAGONAL && !d_state) return DSA_ERR_INVALID_ARG;
+  if (d.state_cap > 0 && !d_state) return DSA_ERR_INVALID_ARG;
   if (plan_bytes < d.plan.bytes) return DSA_ERR_WORKSPACE;
   char* pb = static_cast<char*>(d_plan);
   const char* sb = static_cast<const char*>(d_state);
   dsa::PlanArgs a{};
   a.pos = d_decode_pos;
-  a.st_count = sb ? reinterpret_cast<const int32_t*>(sb + d.state.count_offset) : nullptr;
-  a.st_off = sb ? reinterpret_cast<const uint16_t*>(sb + d.state.offsets_offset) : nullptr;
+  const bool has_state = sb && d.state_cap > 0;
+  a.st_count = has_state ? reinterpret_cast<const int32_t*>(sb + d.state.count_offset) : nullptr;
+  a.st_off = has_state ? reinterpret_cast<const uint16_t*>(sb + d.state.offsets_offset) : nullptr;
   a.count = reinterpret_cast<int32_t*>(pb + d.plan.count_offset);
   a.flags = reinterpret_cast<int32_t*>(pb + d.plan.flags_offset);
   a.idx = reinterpret_cast<int32_t*>(pb + d.plan.indices_offset);
@@ -277,10 +289,11 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
   a.Ldec = d.Ldec;
   a.Nr = d.Nr;
   a.Natt = d.Natt;
+  a.Ns = d.Ns;
   a.mode = d.mode;
   a.plan_cap = d.plan_cap;
   a.state_cap = d.state_cap;
-  a.words = (d.Nr + 31) / 32;
+  a.words = d.words;
   return hip_status(dsa::launch_plan(d, a, stream));
 }
 
@@ -298,20 +311,23 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   dsa_status st = dsa::derive(p, s, &d);
   if (st != DSA_OK) return st;
   if (!d_q || !d_k || !d_v || !kv || !d_decode_pos || !d_out) return DSA_ERR_INVALID_ARG;
-  if (d.mode == DSA_MODE_DIAGONAL && !d_plan) return DSA_ERR_INVALID_ARG;
-  if (fused && d.mode == DSA_MODE_DIAGONAL) {
-    if (!d_state || !d_window_logits) return DSA_ERR_INVALID_ARG;
+  const bool sparse = d.mode != DSA_MODE_DENSE;
+  if (sparse && !d_plan) return DSA_ERR_INVALID_ARG;
+  if (fused && sparse) {
+    if (d.state_cap > 0 && (!d_state || !d_window_logits)) return DSA_ERR_INVALID_ARG;
     if (plan_bytes < d.plan.bytes) return DSA_ERR_WORKSPACE;
-    if (d.Nr > dsa::kMaxFusedWindow) return DSA_ERR_UNSUPPORTED;
+    if (d.state_cap > 0 && d.Nr > dsa::kMaxFusedWindow) return DSA_ERR_UNSUPPORTED;
   }
   if (!std::isfinite(sm_scale)) return DSA_ERR_INVALID_ARG;
   if (kv->stride_row < d.D || kv->stride_head < 0 || kv->stride_batch < 0)
     return DSA_ERR_INVALID_ARG;
   if ((kv->stride_row | kv->stride_head | kv->stride_batch) & 7) return DSA_ERR_INVALID_ARG;
   if (kv->ring_rows < 0 || kv->ring_rows > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
+  // The ring must hold every row a step can read: the sinks plus the window
+  // (sparse modes), or every decode row (dense mode).
   if (kv->ring_rows > 0 &&
-      kv->ring_rows < (d.mode == DSA_MODE_DIAGONAL ? int64_t(d.Nr) : int64_t(d.Ldec)))
-    return DSA_ERR_INVALID_ARG;  // the ring must hold every row the step can read
+      kv->ring_rows < (sparse ? int64_t(d.Ns) + d.Nr : int64_t(d.Ldec)))
+    return DSA_ERR_INVALID_ARG;
   if ((reinterpret_cast<uintptr_t>(d_k) | reinterpret_cast<uintptr_t>(d_v) |
        reinterpret_cast<uintptr_t>(d_q)) & 15)
     return DSA_ERR_INVALID_ARG;
@@ -331,7 +347,7 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   a.scale = sm_scale;
   a.scale_log2 = sm_scale * 1.4426950408889634f;
   a.out = d_out;
-  a.wlog = d.mode == DSA_MODE_DIAGONAL ? d_window_logits : nullptr;
+  a.wlog = sparse ? d_window_logits : nullptr;
   a.part = static_cast<float*>(d_ws);
   a.B = d.B;
   a.Hq = d.Hq;
@@ -342,18 +358,24 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   a.plan_cap = d.plan_cap;
   a.C = d.C;
   a.S = d.S;
-  // A ring of at least L_dec slots maps every position to itself.
-  a.ring = kv->ring_rows >= d.Ldec ? 0 : static_cast<int>(kv->ring_rows);
+  // No ring (0), or a ring of at least L_dec slots, maps every position to
+  // itself; otherwise a.ring >= N_r > 0 slots rotate after the sinks.
+  a.ring = (kv->ring_rows == 0 || kv->ring_rows >= d.Ldec)
+               ? 0
+               : static_cast<int>(kv->ring_rows - d.Ns);
+  a.Ns = d.Ns;
   a.Nr = d.Nr;
   a.Natt = d.Natt;
   a.state_cap = d.state_cap;
-  a.words = (d.Nr + 31) / 32;
-  if (fused && d.mode == DSA_MODE_DIAGONAL) {
+  a.words = d.words;
+  if (fused && sparse) {
     char* sb = static_cast<char*>(d_state);
     char* pbw = static_cast<char*>(const_cast<void*>(d_plan));
-    a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
-    a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
-    a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+    if (d.state_cap > 0) {
+      a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
+      a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
+      a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+    }
     a.plan_count = reinterpret_cast<int32_t*>(pbw + d.plan.count_offset);
     a.plan_flags = reinterpret_cast<int32_t*>(pbw + d.plan.flags_offset);
     a.plan_idx = reinterpret_cast<int32_t*>(pbw + d.plan.indices_offset);
@@ -417,9 +439,9 @@ DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int
   Derived d;
   dsa_status st = dsa::derive(p, s, &d);
   if (st != DSA_OK) return st;
-  if (d.mode != DSA_MODE_DIAGONAL) return DSA_OK;  // dense mode keeps no selection
+  // Dense and window mode keep no selection; nor does N_att - S == N_r.
+  if (d.state_cap == 0) return DSA_OK;
   if (!d_decode_pos || !d_plan || !d_window_logits || !d_state) return DSA_ERR_INVALID_ARG;
-  if (d.state_cap == 0) return DSA_OK;  // N_att == N_r: nothing is ever skipped
   const char* pb = static_cast<const char*>(d_plan);
   char* sb = static_cast<char*>(d_state);
   dsa::SelectArgs a{};
@@ -437,6 +459,7 @@ DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int
   a.Ldec = d.Ldec;
   a.Nr = d.Nr;
   a.Natt = d.Natt;
+  a.Ns = d.Ns;
   a.plan_cap = d.plan_cap;
   a.state_cap = d.state_cap;
   return hip_status(dsa::launch_select(d, a, stream));

@@ -22,8 +22,9 @@
 //     kept positions of a window tile are held one per lane and handed to
 //     the row groups with ds_bpermute, prompt tiles need none;
 //   - K/V rows are loaded with the non-temporal hint (streamed once);
-//   - with a ring layout a kept decode position j is read from slot
-//     j mod ring (the ring holds the live window; evicted rows are gone);
+//   - with a ring layout a kept decode position j >= S (S sinks) is read
+//     from slot S + (j - S) mod (ring - S) (the ring holds the sinks and the
+//     live window; evicted rows are gone);
 //   - a workgroup has as many waves (1..4) as its split has tiles, so no wave
 //     sits idle holding registers;
 //   - q.k partial sums are reduced inside the row's lane group with DPP row
@@ -43,7 +44,9 @@
 // split covers the whole (request, KV head) the same workgroup then runs the
 // phase-2 argmin on the window logits it computed and appends the skip entry.
 // Every value it produces is bit-identical to dsa_plan -> dsa_decode_attention
-// -> dsa_select.
+// -> dsa_select.  The same path serves the sink variants of section 5.1: the
+// S sinks are the first S kept ranks, the window rule applies to the later
+// positions, and window mode (no stored offsets) skips the bitmap.
 #include <hip/hip_ext.h>
 
 #include "device.h"
@@ -89,7 +92,9 @@ __device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pa
 // bitmap of the first nuse stored offsets, plus the ranking cursor.
 struct SkipSet {
   uint32_t* bm;
-  int t, dmax;
+  int t, dmax;   // window offsets 0 .. dmax (dmax < 0: no window yet)
+  int sk;        // sinks kept ahead of the window: min(S, t + 1)
+  bool any;      // the bitmap holds at least one skipped offset
   int p0, rank;  // next candidate chunk and kept positions before it
   int flags;
 };
@@ -108,7 +113,7 @@ struct StateRegs {
 
 __device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, StateRegs& sr) {
   const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-  sr.cnt = a.st_count[pair];
+  sr.cnt = a.state_cap > 0 ? a.st_count[pair] : 0;
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
     const int e = lane + 64 * i;
@@ -141,14 +146,17 @@ __device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, u
   fence_wave();
   ss.bm = bm;
   ss.t = t;
-  ss.dmax = min(t, a.Nr - 1);
+  ss.sk = min(a.Ns, t + 1);
+  ss.dmax = min(t - a.Ns, a.Nr - 1);
+  ss.any = nuse > 0;
   ss.p0 = t - ss.dmax;
-  ss.rank = 0;
+  ss.rank = ss.sk;
   ss.flags = flags;
 }
 
 __device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
   if (p > ss.t) return false;
+  if (!ss.any) return true;
   const int d = ss.t - p;
   return ((ss.bm[d >> 5] >> (d & 31)) & 1u) == 0u;
 }
@@ -160,6 +168,10 @@ __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss
                             int* kp, int kp_base) {
   const uint64_t below = (uint64_t(1) << lane) - 1;
   int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
+  for (int r = lo + lane; r < min(hi, ss.sk); r += 64) {  // sink rank r is position r
+    kp[r - kp_base] = r;
+    plan[r] = r;
+  }
   while (ss.p0 <= ss.t && ss.rank < hi) {
     const int p = ss.p0 + lane;
     const bool kept = is_kept(ss, p);
@@ -179,7 +191,7 @@ __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss
 
 // Total kept positions of the window (for the DSA_FLAG_COUNT check).
 __device__ int count_kept(const SkipSet& ss, int lane) {
-  int n = 0;
+  int n = ss.sk;
   for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64) n += __popcll(__ballot(is_kept(ss, p0 + lane)));
   return n;
 }
@@ -437,7 +449,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       } else {
         if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
       }
-      if (a.ring) pos_l %= a.ring;  // decode position -> ring slot
+      if (a.ring && pos_l >= a.Ns) pos_l = a.Ns + (pos_l - a.Ns) % a.ring;  // ring slot
     }
     if constexpr (MF) {
       mfma_tile<D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, m_c, l_c,
@@ -571,18 +583,21 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
 
   if constexpr (FUSED) {
     // Phase-2 selection, when this workgroup saw every kept window key.
-    if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr - 2) {
+    // The sinks (the first Ns kept ranks) are never candidates.
+    if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr + a.Ns - 2) {
       const int k = rr.t - (a.Natt - 1);
       if (k < a.state_cap) {
         const int cnt = a.st_count[pair];
         if (cnt < k) {
           if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
         } else {
-          const int nwin = n - a.Lp;
-          int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl_s[g][j]; });
+          const int nwin = n - a.Lp - a.Ns;
+          const int ns = a.Ns;
+          int jbest =
+              window_argmin<G>(lane, nwin, [&](int g, int j) { return wl_s[g][ns + j]; });
           if (lane == 0) {
             if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-            const int d = min(max(rr.t - kp_s[jbest], 0), a.Nr - 2);
+            const int d = min(max(rr.t - kp_s[ns + jbest], 0), a.Nr - 2);
             a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
             a.st_count[pair] = k + 1;
           }
@@ -713,7 +728,7 @@ __global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
   for (int g = wave; g < G; g += kWaves) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
   if (wave != kWaves - 1) return;
   const int t = rr.t;
-  if (t < a.Natt - 1 || t > a.Nr - 2) return;
+  if (t < a.Natt - 1 || t > a.Nr + a.Ns - 2) return;
   const int k = t - (a.Natt - 1);
   if (k >= a.state_cap) return;
   const int cnt = a.st_count[pair];
@@ -721,13 +736,13 @@ __global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
     if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
     return;
   }
-  const int nwin = rr.n - a.Lp;
-  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap;
+  const int nwin = rr.n - a.Lp - a.Ns;  // window keys after the sinks
+  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap + a.Ns;
   const int plan_cap = a.plan_cap;
   int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl[g * plan_cap + j]; });
   if (lane == 0) {
     if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-    const int pos = a.plan_idx[static_cast<size_t>(pair) * a.plan_cap + jbest];
+    const int pos = a.plan_idx[static_cast<size_t>(pair) * a.plan_cap + a.Ns + jbest];
     const int d = min(max(t - pos, 0), a.Nr - 2);
     a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
     a.st_count[pair] = k + 1;

@@ -14,9 +14,12 @@ namespace dsa {
 // Everything a call needs, derived once from (params, shape) on the host.
 struct Derived {
   int B, Hq, Hkv, G, D;
-  int Lp, Ldec, Nr, Natt, mode;
+  int Lp, Ldec, Natt, mode;
+  int Ns;         // sink positions kept ahead of the window (0 in dense mode)
+  int Nr;         // window W after the sinks: N_r (diagonal), N_att - S (window mode)
   int plan_cap;   // kept decode rows per (request, KV head): min(N_att, L_dec), 0 when dense
-  int state_cap;  // skip entries per (request, KV head): N_r - N_att
+  int state_cap;  // skip entries per (request, KV head): W - (N_att - S) in diagonal mode, else 0
+  int words;      // 32-bit words of a skip bitmap over W offsets (0 without a state)
   dsa_plan_layout plan;
   dsa_state_layout state;
   int rows_max;   // prompt rows + the most decode rows one request can attend
@@ -44,7 +47,7 @@ struct PlanArgs {
   int32_t* count;
   int32_t* flags;
   int32_t* idx;
-  int pairs, Hkv, Ldec, Nr, Natt, mode, plan_cap, state_cap, words;
+  int pairs, Hkv, Ldec, Nr, Natt, Ns, mode, plan_cap, state_cap, words;
 };
 
 struct DecodeArgs {
@@ -62,7 +65,8 @@ struct DecodeArgs {
   float* wlog;           // window logits or nullptr
   float* part;           // split partials (S > 1)
   int B, Hq, Hkv, Lp, Ldec, mode, plan_cap, C, S;
-  int ring;              // decode rows in a ring of this many slots (0: linear)
+  int ring;              // positions >= Ns rotate through this many slots (0: linear)
+  int Ns;                // sink positions
   // fused step only: selection state (in/out) and plan (out)
   int32_t* st_count;
   int32_t* st_flags;
@@ -81,7 +85,7 @@ struct SelectArgs {
   int32_t* st_count;
   int32_t* st_flags;
   uint16_t* st_off;
-  int pairs, Hq, Hkv, G, Ldec, Nr, Natt, plan_cap, state_cap;
+  int pairs, Hq, Hkv, G, Ldec, Nr, Natt, Ns, plan_cap, state_cap;
 };
 
 struct ResetArgs {

@@ -8,6 +8,12 @@
 // with n = clamp(t - N_att + 1, 0, N_r - N_att) entries appended at earlier
 // steps.  d <= N_r - 1 is the live window [t - N_r + 1, t]: in phase 3 row
 // t - N_r is evicted in the same step, so it is never attended.
+//
+// With S sinks (section 5.1) positions 0 .. S-1 are kept first and the rule
+// above applies to the later positions with t - S in place of t and
+// N_att - S in place of N_att: offsets 0 .. min(t - S, W - 1), the first
+// clamp(t - N_att + 1, 0, cap) stored offsets skipped.  Window mode is the
+// same with W = N_att - S and no stored offsets.
 #include "device.h"
 #include "internal.h"
 
@@ -25,16 +31,17 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
   // Every load of the wave is issued before any of them is used: the
   // decode position, the stored count and the first kPre*64 stored offsets
   // (entries past the count are ignored).
-  const bool diag = a.mode == DSA_MODE_DIAGONAL;
+  const bool sparse = a.mode != DSA_MODE_DENSE;
+  const bool stated = a.state_cap > 0;  // diagonal mode with a skip list
   const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
   int t = live ? a.pos[pair / a.Hkv] : -1;
-  const int cnt = (live && diag) ? a.st_count[pair] : 0;
+  const int cnt = (live && stated) ? a.st_count[pair] : 0;
   constexpr int kPre = 8;
   int dv[kPre];
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
     const int e = lane + 64 * i;
-    dv[i] = (live && diag && e < a.state_cap) ? off[e] : 0;
+    dv[i] = (live && stated && e < a.state_cap) ? off[e] : 0;
   }
   int flags = 0, nuse = 0;
   if (live) {
@@ -45,16 +52,14 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
       flags = DSA_FLAG_POS_CLAMPED;
     }
   }
-  if (live && diag && t >= 0) {
+  if (live && stated && t >= 0) {
     const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
     if (cnt < nvalid) flags |= DSA_FLAG_STATE_BEHIND;
     nuse = min(max(cnt, 0), nvalid);
   }
-  if (diag) {
-    for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
-  }
+  for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
   __syncthreads();
-  if (diag && live && t >= 0) {
+  if (nuse > 0) {
     bool bad = false;
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
@@ -80,7 +85,7 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
     }
     return;
   }
-  if (!diag) {
+  if (!sparse) {
     if (lane == 0) {
       a.count[pair] = t + 1;
       a.flags[pair] = flags;
@@ -88,17 +93,20 @@ __global__ __launch_bounds__(kBlock) void plan_kernel(PlanArgs a) {
     return;
   }
 
-  // Ascending positions p = t - d for d = dmax .. 0, compacted by ballot.
-  const int dmax = min(t, a.Nr - 1);
+  // The sinks, then ascending positions p = t - d for d = dmax .. 0,
+  // compacted by ballot (dmax < 0 while t < S: no window yet).
+  const int sk = min(a.Ns, t + 1);
+  const int dmax = min(t - a.Ns, a.Nr - 1);
   int32_t* out = a.idx + static_cast<size_t>(pair) * a.plan_cap;
+  for (int r = lane; r < sk; r += 64) out[r] = r;
   const uint64_t below = (uint64_t(1) << lane) - 1;
-  int n = 0;
+  int n = sk;
   for (int p0 = t - dmax; p0 <= t; p0 += 64) {
     const int p = p0 + lane;
     bool kept = false;
     if (p <= t) {
       const int d = t - p;
-      kept = ((bm[d >> 5] >> (d & 31)) & 1u) == 0u;
+      kept = nuse == 0 || ((bm[d >> 5] >> (d & 31)) & 1u) == 0u;
     }
     const uint64_t mask = __ballot(kept);
     const int slot = n + __popcll(mask & below);
@@ -126,7 +134,7 @@ __global__ __launch_bounds__(256) void reset_kernel(ResetArgs a) {
 hipError_t launch_plan(const Derived& d, const PlanArgs& a, hipStream_t st) {
   const int pairs = d.B * d.Hkv;
   const int grid = (pairs + kWaves - 1) / kWaves;
-  const size_t lds = d.mode == DSA_MODE_DIAGONAL ? sizeof(uint32_t) * kWaves * a.words : 0;
+  const size_t lds = sizeof(uint32_t) * kWaves * a.words;
   plan_kernel<<<grid, kBlock, lds, st>>>(a);
   return hipGetLastError();
 }

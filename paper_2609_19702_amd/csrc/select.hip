@@ -8,6 +8,10 @@
 // the softmax orders identically.  Ties go to the first (oldest) key.  The
 // entry is stored as the offset t - idx[j*] at list slot k = t - N_att + 1,
 // so running the same step twice rewrites the same slot.
+//
+// With S sinks the steps that select are N_att - 1 <= t <= N_r + S - 2 (the
+// phase-2 range of the positions after the sinks), the sinks are the first
+// S kept positions and never candidates, and k = t - N_att + 1 still holds.
 #include "device.h"
 #include "internal.h"
 
@@ -26,20 +30,21 @@ __global__ __launch_bounds__(kBlock) void select_kernel(SelectArgs a) {
   const int n = min(max(a.count[pair], 0), a.plan_cap);
   if (t < 0) return;
   t = min(t, a.Ldec - 1);
-  if (t < a.Natt - 1 || t > a.Nr - 2) return;
+  if (t < a.Natt - 1 || t > a.Nr + a.Ns - 2) return;
   const int k = t - (a.Natt - 1);
   if (k >= a.state_cap) return;
   if (cnt < k) {
     if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
     return;
   }
-  if (n == 0) return;
-  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap;
+  const int nw = n - a.Ns;  // kept window keys after the sinks
+  if (nw <= 0) return;
+  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap + a.Ns;
   const int plan_cap = a.plan_cap;
-  int jbest = window_argmin<G>(lane, n, [&](int g, int j) { return wl[g * plan_cap + j]; });
+  int jbest = window_argmin<G>(lane, nw, [&](int g, int j) { return wl[g * plan_cap + j]; });
   if (lane == 0) {
-    if (jbest < 0 || jbest >= n) jbest = 0;  // only for NaN logits
-    const int pos = a.idx[static_cast<size_t>(pair) * a.plan_cap + jbest];
+    if (jbest < 0 || jbest >= nw) jbest = 0;  // only for NaN logits
+    const int pos = a.idx[static_cast<size_t>(pair) * a.plan_cap + a.Ns + jbest];
     const int d = min(max(t - pos, 0), a.Nr - 2);
     a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
     a.st_count[pair] = k + 1;

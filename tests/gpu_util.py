@@ -24,14 +24,19 @@ def say(*a):
 
 def states_to_buffer(p, s, states, t_list, device=DEV):
     """Library state buffer holding the oracle states ``states[b][h]`` (each
-    after steps ``0 .. t_list[b]-1``)."""
+    after steps ``0 .. t_list[b]-1``).  With sinks the oracle's state counts
+    steps from the first position after the sinks; offsets are the same in
+    both frames."""
     buf = torch.zeros(B.state_bytes(p, s), dtype=torch.uint8)
+    if B.state_layout(p, s).cap == 0:  # nothing is ever selected: empty lists
+        return buf.to(device)
     cnt, flg, off = B.state_views(p, s, buf)
     Hkv = s.num_kv_heads
     for b, per_head in enumerate(states):
         for h, st in enumerate(per_head):
             pair = b * Hkv + h
-            d = alg1.offsets_of(st, t_list[b] - 1) if t_list[b] > 0 else []
+            t_state = t_list[b] - p.sinks  # steps the state has seen
+            d = alg1.offsets_of(st, t_state - 1) if t_state > 0 else []
             assert len(d) == len(st.skip_idx)
             cnt[pair] = len(d)
             if d:
@@ -49,14 +54,12 @@ def run_layer(p, s, q, kv, pos, state=None, bufs=None, logits=True, stream=None)
     """plan + decode (+ combine) for one layer; returns the buffers."""
     if bufs is None:
         bufs = B.alloc_buffers(p, s, DEV)
-    if p.mode == B.MODE_DIAGONAL:
-        B.plan(p, s, pos, state, bufs.plan, stream=stream)
-    else:
-        B.plan(p, s, pos, None, bufs.plan, stream=stream)
+    sparse = p.mode != B.MODE_DENSE
+    B.plan(p, s, pos, state if sparse else None, bufs.plan, stream=stream)
     B.decode_attention(p, s, q, kv.k, kv.v, B.kv_layout(kv.k), pos,
-                       bufs.plan if p.mode == B.MODE_DIAGONAL else None,
+                       bufs.plan if sparse else None,
                        1.0 / math.sqrt(s.head_dim), bufs.out,
-                       bufs.logits if (logits and p.mode == B.MODE_DIAGONAL) else None,
+                       bufs.logits if (logits and sparse) else None,
                        bufs.workspace, stream=stream)
     return bufs
 

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.SIGNATURES), "binding and header disagree"
-    assert B.abi_version() == 1
+    assert B.abi_version() == 2
 
 
 def test_status_strings():
@@ -52,9 +52,25 @@ def test_default_window():
     assert p.window == oparams.default_window(24, 24)
 
 
+def test_params_from_sparsity_sink_modes():
+    # window mode: the recent window is not bounded by N_r
+    p = B.params_from_sparsity(0, 24, 24, 0, 200, mode=B.MODE_WINDOW, sinks=4)
+    assert (p.n_att, p.sinks, p.mode) == (oparams.n_att_from_sparsity(24, 24, 576, 200), 4, 2)
+    p = B.params_from_sparsity(0, 24, 24, 0, 200, mode=B.MODE_DIAGONAL, sinks=4)
+    assert p.n_att == 288 and p.window == 288
+    # at least one window token after the sinks
+    p = B.params_from_sparsity(0, 4, 4, 8, 1000, mode=B.MODE_DIAGONAL, sinks=4)
+    assert p.n_att == 5
+    with pytest.raises(B.DSAError):
+        B.params_from_sparsity(0, 4, 4, 4, 950, mode=B.MODE_DIAGONAL, sinks=4)
+    with pytest.raises(B.DSAError):
+        B.params_from_sparsity(0, 4, 4, 4, 950, mode=B.MODE_WINDOW, sinks=-1)
+
+
 @pytest.mark.parametrize("bad", [
     dict(prompt_len=-1), dict(grid_h=0), dict(window=0), dict(window=70000), dict(n_att=0),
-    dict(n_att=200), dict(mode=2),
+    dict(n_att=200), dict(mode=3), dict(sinks=-1), dict(sinks=8), dict(mode=2, sinks=9),
+    dict(mode=2, n_att=(1 << 24) + 1),
 ])
 def test_validate_rejects_bad_params(bad):
     kw = dict(prompt_len=8, grid_h=8, grid_w=8, window=32, n_att=8, mode=1)
@@ -62,6 +78,13 @@ def test_validate_rejects_bad_params(bad):
     p = B.make_params(**kw)
     assert B.validate(p, B.make_shape(2, 4, 4, 64)) == B.ERR_INVALID_ARG
     assert B.plan_bytes(p, B.make_shape(2, 4, 4, 64)) == 0
+
+
+def test_validate_sink_modes():
+    s = B.make_shape(2, 4, 4, 64)
+    assert B.validate(B.make_params(8, 8, 8, 32, 8, 1, sinks=7), s) == B.OK
+    assert B.validate(B.make_params(8, 8, 8, 32, 200, 2, sinks=4), s) == B.OK  # n_att > N_r
+    assert B.validate(B.make_params(8, 8, 8, 32, 8, 0, sinks=50), s) == B.OK   # dense ignores it
 
 
 def test_validate_shapes():
@@ -74,7 +97,7 @@ def test_validate_shapes():
     assert B.validate(p, B.make_shape(2, 12, 4, 64)) == B.ERR_UNSUPPORTED  # group 3
 
 
-@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("mode,sinks", [(0, 0), (1, 0), (1, 4), (2, 4), (2, 0)])
 @pytest.mark.parametrize("shape,par", [
     ((64, 20, 20, 64), (120, 24, 24, 128, 950)),
     ((128, 32, 32, 128), (256, 24, 24, 256, 950)),
@@ -83,14 +106,14 @@ def test_validate_shapes():
     ((256, 32, 32, 128), (256, 96, 96, 1024, 950)),
     ((3, 8, 1, 64), (0, 5, 7, 9, 500)),
 ])
-def test_layouts_and_split_config(mode, shape, par):
-    p = B.params_from_sparsity(*par, mode=mode)
+def test_layouts_and_split_config(mode, sinks, shape, par):
+    p = B.params_from_sparsity(*par, mode=mode, sinks=sinks)
     s = B.make_shape(*shape)
     pairs = s.batch * s.num_kv_heads
     pl, sl, li = B.plan_layout(p, s), B.state_layout(p, s), B.launch_info(p, s)
     L_dec = p.grid_h * p.grid_w
-    assert pl.cap == (min(p.n_att, L_dec) if mode == 1 else 0)
-    assert sl.cap == p.window - p.n_att
+    assert pl.cap == (min(p.n_att, L_dec) if mode else 0)
+    assert sl.cap == (p.window - (p.n_att - sinks) if mode == 1 else 0)
     for off in (pl.count_offset, pl.flags_offset, pl.indices_offset,
                 sl.count_offset, sl.flags_offset, sl.offsets_offset):
         assert off % 256 == 0
@@ -98,7 +121,7 @@ def test_layouts_and_split_config(mode, shape, par):
     assert pl.indices_offset >= pl.flags_offset + 4 * pairs
     assert pl.bytes == B.plan_bytes(p, s) and pl.bytes >= pl.indices_offset + 4 * pairs * pl.cap
     assert sl.bytes == B.state_bytes(p, s) and sl.bytes >= sl.offsets_offset + 2 * pairs * sl.cap
-    rows_max = p.prompt_len + (pl.cap if mode == 1 else L_dec)
+    rows_max = p.prompt_len + (pl.cap if mode else L_dec)
     block = 32 if li.kernel_variant == 100 else (512 // s.head_dim) * li.kernel_variant
     assert (li.kernel_variant == 100) == (s.num_q_heads > s.num_kv_heads)
     assert 1 <= li.waves_per_group <= 4

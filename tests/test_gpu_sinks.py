@@ -1,0 +1,248 @@
+"""GPU parity of the sink variants of section 5.1 against the oracle:
+Diagonal+Sink (diagonal mode with S sinks) and StreamingLLM / the sliding
+window (window mode with S sinks, or none).
+
+* plans from oracle-drawn selection histories, at the positions where the
+  rules change (before, at and after the sinks, the phase boundaries of
+  the shifted algorithm), bit for bit;
+* lockstep trajectories over a whole tiny image: kept sets bit for bit,
+  outputs within the tolerance, phase-2 choices equal to the oracle's argmin
+  or inside the fp32 rounding band of it; the fused step reproduces the
+  three separate calls bit for bit at every step;
+* the ring layout with pinned sink rows gives the linear cache's results
+  bit for bit;
+* window mode needs no selection state or logits buffer."""
+
+import copy
+import math
+import random
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import step as ostep
+from paper_2609_19702_amd import binding as B
+from paper_2609_19702_amd import synth
+from tests.gpu_util import DEV, TOL, offsets_from_buffer, rel_err, say, states_to_buffer, within_tie_band
+
+pytestmark = pytest.mark.gpu
+
+ORACLE_MODE = {B.MODE_DIAGONAL: "diagonal_sink", B.MODE_WINDOW: "streaming"}
+
+
+def edge_positions(L_dec, N_r, N_att, S):
+    ts = {0, S - 1, S, S + 1, N_att - 2, N_att - 1, N_att, N_r + S - 2, N_r + S - 1, N_r + S,
+          L_dec - 1, L_dec // 2}
+    return sorted(t for t in ts if 0 <= t < L_dec)
+
+
+PLAN_CASES = [
+    # mode, B, Hkv, L_p, gh, gw, N_r, N_att, S
+    (B.MODE_DIAGONAL, 4, 4, 32, 16, 16, 64, 13, 4),
+    (B.MODE_DIAGONAL, 3, 2, 0, 7, 9, 20, 5, 4),
+    (B.MODE_DIAGONAL, 2, 3, 5, 8, 8, 16, 16, 4),
+    (B.MODE_DIAGONAL, 2, 2, 120, 24, 24, 288, 29, 4),
+    (B.MODE_DIAGONAL, 2, 2, 7, 12, 12, 70, 9, 8),
+    (B.MODE_WINDOW, 4, 4, 32, 16, 16, 64, 13, 4),
+    (B.MODE_WINDOW, 3, 2, 0, 24, 24, 288, 200, 4),
+    (B.MODE_WINDOW, 2, 2, 9, 9, 9, 5, 7, 0),
+]
+
+
+@pytest.mark.parametrize("case", PLAN_CASES, ids=[str(c) for c in PLAN_CASES])
+def test_sink_plan_matches_oracle(case):
+    mode, Bn, Hkv, Lp, gh, gw, N_r, N_att, S = case
+    L_dec = gh * gw
+    say("sink plan case", case)
+    rng = random.Random(hash(case) & 0xFFFF)
+    W = N_r if mode == B.MODE_DIAGONAL else N_att - S
+    edges = edge_positions(L_dec, W, N_att, S)
+    t_list = [edges[i % len(edges)] if i < len(edges) else rng.randrange(L_dec)
+              for i in range(max(2 * Bn, len(edges)))]
+    p = B.make_params(Lp, gh, gw, N_r, N_att, mode, S)
+    s = B.make_shape(Bn, Hkv, Hkv, 64)
+    om = ORACLE_MODE[mode]
+    for rep in range(0, len(t_list), Bn):
+        ts = (t_list[rep:rep + Bn] + [0] * Bn)[:Bn]
+        states = [ostep.random_states(Hkv, N_r, N_att, t, [rng.randrange(1 << 30) for _ in range(Hkv * (N_r + S))],
+                                      om, S) for t in ts]
+        plan = torch.zeros(B.plan_bytes(p, s), dtype=torch.uint8, device=DEV)
+        pos = torch.tensor(ts, dtype=torch.int32, device=DEV)
+        st_buf = states_to_buffer(p, s, states, ts) if mode == B.MODE_DIAGONAL else None
+        B.plan(p, s, pos, st_buf, plan)
+        cnt, flg, idx = (x.cpu().numpy() for x in B.plan_views(p, s, plan))
+        for b, t in enumerate(ts):
+            for h in range(Hkv):
+                rec = ostep.kept_with_sinks(t, S, copy.deepcopy(states[b][h]), lambda t_, i_: 0)
+                pair = b * Hkv + h
+                assert flg[pair] == 0, (b, h, t, flg[pair])
+                assert cnt[pair] == len(rec.idx) == min(t + 1, N_att)
+                assert idx[pair, :cnt[pair]].tolist() == rec.idx, (b, h, t)
+
+
+def lockstep(mode, Hq, Hkv, d, Lp, gh, gw, N_r, N_att, S, seed):
+    """Whole-image trajectory of one request: separate calls checked against
+    the oracle, fused step checked against the separate calls."""
+    w = synth.Workload("sink_traj", 1, 1, Hq, Hkv, d, Lp, gh, gw, N_r, outlier_frac=0.01, seed=seed)
+    kv = synth.layer_kv(w, 0, DEV)
+    L = gh * gw
+    Q = torch.stack([synth.step_query(w, 0, t)[0] for t in range(L)])
+    p = B.make_params(Lp, gh, gw, N_r, N_att, mode, S)
+    s = B.make_shape(1, Hq, Hkv, d)
+    bufs, fb = B.alloc_buffers(p, s, DEV), B.alloc_buffers(p, s, DEV)
+    B.state_reset(p, s, bufs.state)
+    scale = 1 / math.sqrt(d)
+    k64 = kv.k[0].to(torch.float64).cpu().numpy()
+    v64 = kv.v[0].to(torch.float64).cpu().numpy()
+    Kp, Vp, K, V = k64[:, :Lp], v64[:, :Lp], k64[:, Lp:], v64[:, Lp:]
+    Q64 = Q.to(torch.float64).numpy()
+    om = ORACLE_MODE[mode]
+    states = ostep.new_states(Hkv, N_r, N_att, om, S)
+    g = Hq // Hkv
+    forced, worst = 0, 0.0
+    lay = B.kv_layout(kv.k)
+    for t in range(L):
+        pos = torch.tensor([t], dtype=torch.int32, device=DEV)
+        q = Q[t].unsqueeze(0).contiguous().to(DEV)
+        fb.state.copy_(bufs.state)
+        B.decode_step(p, s, q, kv.k, kv.v, lay, pos, fb.state, fb.plan, scale, fb.out, fb.logits,
+                      fb.workspace)
+        B.plan(p, s, pos, bufs.state, bufs.plan)
+        B.decode_attention(p, s, q, kv.k, kv.v, lay, pos, bufs.plan, scale, bufs.out, bufs.logits,
+                           bufs.workspace)
+        B.select(p, s, pos, bufs.plan, bufs.logits, bufs.state)
+        torch.cuda.synchronize()
+        assert torch.equal(fb.out, bufs.out) and torch.equal(fb.state, bufs.state), t
+        assert torch.equal(fb.plan, bufs.plan), t
+        cnt, flg, idx = (x.cpu().numpy() for x in B.plan_views(p, s, bufs.plan))
+        scnt, sflg, soff = offsets_from_buffer(p, s, bufs.state)
+        out = bufs.out.cpu().numpy().astype(np.float64)[0]
+
+        def decide(kvh, t_, idx_, j_ref, sigma):
+            nonlocal forced
+            k = t_ - (N_att - 1)
+            assert scnt[kvh] == k + 1, (t_, kvh, scnt[kvh])
+            j_gpu = idx_.index(t_ - int(soff[kvh, k]))
+            if j_gpu != j_ref:
+                qg = Q64[t_][kvh * g:(kvh + 1) * g]
+                assert within_tie_band(qg, K[kvh][idx_], scale, j_gpu, j_ref), (t_, kvh)
+                forced += 1
+            return j_gpu
+
+        res = ostep.request_step(t, Q64[t], Kp, Vp, K, V, scale, om, states, decide, S)
+        logits = bufs.logits.view(Hq, -1).cpu().numpy()
+        for h in range(Hkv):
+            assert flg[h] == 0 and sflg[h] == 0
+            assert idx[h, :cnt[h]].tolist() == res.heads[h].idx, (t, h)
+            wl = res.heads[h].window_logits
+            got = logits[h * g:(h + 1) * g, :cnt[h]]
+            assert np.abs(got - wl).max() <= 1e-4 * max(1.0, np.abs(wl).max()), (t, h)
+        for h in range(Hq):
+            e = rel_err(out[h], res.out[h])
+            worst = max(worst, e)
+            assert e <= TOL, (t, h, e)
+    return forced, worst
+
+
+TRAJ = [
+    # mode, Hq, Hkv, d, L_p, gh, gw, N_r, N_att, S
+    (B.MODE_DIAGONAL, 8, 8, 64, 32, 16, 16, 64, 13, 4),
+    (B.MODE_DIAGONAL, 8, 2, 128, 16, 8, 8, 24, 10, 4),
+    (B.MODE_WINDOW, 8, 8, 64, 32, 16, 16, 64, 13, 4),
+    (B.MODE_WINDOW, 16, 2, 64, 8, 10, 10, 8, 20, 0),
+]
+
+
+@pytest.mark.parametrize("case", TRAJ, ids=[str(c) for c in TRAJ])
+def test_sink_trajectory(case):
+    say("sink trajectory", case)
+    forced, worst = lockstep(*case, seed=6)
+    say(f"  forced near-tie choices: {forced}, worst rel err {worst:.2e}")
+    assert forced <= 2
+
+
+def to_ring(kv, Lp, ts, R, S):
+    k = kv.k[:, :, :Lp + R].clone()
+    v = kv.v[:, :, :Lp + R].clone()
+    k[:, :, Lp:] = 1e4
+    v[:, :, Lp:] = -1e4
+    for b, t in enumerate(ts):
+        for j in list(range(min(S, t + 1))) + list(range(max(S, t - (R - S) + 1), t + 1)):
+            slot = j if j < S else S + (j - S) % (R - S)
+            k[b, :, Lp + slot] = kv.k[b, :, Lp + j]
+            v[b, :, Lp + slot] = kv.v[b, :, Lp + j]
+    return k, v
+
+
+@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("case", [
+    # mode, B, Hq, Hkv, d, L_p, gh, gw, N_r, N_att, S, ring
+    (B.MODE_DIAGONAL, 6, 8, 8, 64, 20, 12, 12, 40, 10, 4, 44),
+    (B.MODE_DIAGONAL, 5, 8, 2, 128, 0, 10, 10, 30, 7, 4, 39),
+    (B.MODE_WINDOW, 6, 8, 8, 64, 20, 12, 12, 40, 10, 4, 10),
+    (B.MODE_WINDOW, 5, 16, 2, 64, 3, 10, 10, 30, 12, 0, 15),
+])
+def test_sink_ring_equals_linear(case, fused):
+    mode, Bn, Hq, Hkv, d, Lp, gh, gw, N_r, N_att, S, R = case
+    say("sink ring", case, "fused" if fused else "separate")
+    rng = random.Random(R * 13 + Bn)
+    L = gh * gw
+    ts = [L - 1, S, N_att - 1, max(S - 1, 0)] + [rng.randrange(L) for _ in range(Bn - 4)]
+    w = synth.Workload("sink_ring", 1, Bn, Hq, Hkv, d, Lp, gh, gw, N_r, outlier_frac=0.01)
+    kv = synth.layer_kv(w, 0, DEV)
+    q = synth.layer_query(w, 0, DEV)
+    p = B.make_params(Lp, gh, gw, N_r, N_att, mode, S)
+    s = B.make_shape(Bn, Hq, Hkv, d)
+    om = ORACLE_MODE[mode]
+    states = [ostep.random_states(Hkv, N_r, N_att, t, [rng.randrange(1 << 30) for _ in range(Hkv * (N_r + S))],
+                                  om, S) for t in ts]
+    st0 = states_to_buffer(p, s, states, ts) if mode == B.MODE_DIAGONAL else None
+    pos = torch.tensor(ts, dtype=torch.int32, device=DEV)
+    rk, rv = to_ring(kv, Lp, ts, R, S)
+    results = []
+    for k, v, ring in ((kv.k, kv.v, 0), (rk, rv, R)):
+        bufs = B.alloc_buffers(p, s, DEV)
+        st = st0.clone() if st0 is not None else None
+        lay = B.kv_layout(k, ring_rows=ring)
+        if fused:
+            B.decode_step(p, s, q, k, v, lay, pos, st, bufs.plan, 0.125, bufs.out, bufs.logits,
+                          bufs.workspace)
+        else:
+            B.plan(p, s, pos, st, bufs.plan)
+            B.decode_attention(p, s, q, k, v, lay, pos, bufs.plan, 0.125, bufs.out, bufs.logits,
+                               bufs.workspace)
+            B.select(p, s, pos, bufs.plan, bufs.logits, st)
+        torch.cuda.synchronize()
+        results.append((bufs.out.clone(), None if st is None else st.clone(), bufs.plan.clone()))
+    (o0, s0, p0), (o1, s1, p1) = results
+    assert torch.isfinite(o1).all()
+    assert torch.equal(o0, o1)
+    assert s0 is None or torch.equal(s0, s1)
+    assert torch.equal(p0, p1)
+    r_min = S + N_r if mode == B.MODE_DIAGONAL else N_att  # the sinks plus the window
+    with pytest.raises(B.DSAError) as e:
+        B.decode_attention(p, s, q, rk, rv, B.kv_layout(rk, ring_rows=r_min - 1), pos, bufs.plan,
+                           0.125, bufs.out, None, bufs.workspace)
+    assert e.value.status == B.ERR_INVALID_ARG
+
+
+def test_window_mode_needs_no_state():
+    p = B.make_params(16, 12, 12, 40, 20, B.MODE_WINDOW, 4)
+    s = B.make_shape(3, 8, 2, 64)
+    assert B.state_layout(p, s).cap == 0
+    w = synth.Workload("win_nostate", 1, 3, 8, 2, 64, 16, 12, 12, 40, outlier_frac=0.01)
+    kv = synth.layer_kv(w, 0, DEV)
+    q = synth.layer_query(w, 0, DEV)
+    pos = torch.tensor([143, 3, 60], dtype=torch.int32, device=DEV)
+    a, b = B.alloc_buffers(p, s, DEV), B.alloc_buffers(p, s, DEV)
+    lay = B.kv_layout(kv.k)
+    B.decode_step(p, s, q, kv.k, kv.v, lay, pos, None, a.plan, 0.125, a.out, None, a.workspace)
+    B.plan(p, s, pos, None, b.plan)
+    B.decode_attention(p, s, q, kv.k, kv.v, lay, pos, b.plan, 0.125, b.out, None, b.workspace)
+    B.select(p, s, pos, b.plan, None, None)
+    torch.cuda.synchronize()
+    assert torch.equal(a.out, b.out) and torch.equal(a.plan, b.plan)
+    cnt, flg, idx = (x.cpu() for x in B.plan_views(p, s, b.plan))
+    assert cnt.tolist() == [20, 20, 4, 4, 20, 20] and not flg.any()
+    assert idx[0].tolist() == [0, 1, 2, 3] + list(range(128, 144))
