@@ -11,7 +11,9 @@ one pass; ``value``), and for comparison the same work as three calls
 once as a HIP graph and replayed (``--eager`` launches it from Python
 instead).  The dense mode of the
 same kernels, on the same inputs and positions, is timed alongside for the
-speedup.  Prints one JSON line.
+speedup, and so are the fused steps of the sink variants of section 5.1 at
+the same budget N_att (Diagonal+Sink4, and StreamingLLM: 4 sinks plus a
+recent window, no selection).  Prints one JSON line.
 
 ``roofline`` describes the decode kernel (the dominant one): algorithmic K/V
 bytes per launch (4*d bytes per attended key per KV head) divided by its
@@ -48,7 +50,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--only", default=None, choices=["fused", "separate", "dense"],
+    ap.add_argument("--only", default=None,
+                    choices=["fused", "separate", "dense", "diag_sink4", "streaming"],
                     help="time one step variant only (shorter profiler runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                     help="run a plain device copy of MB megabytes 10 times and exit (the "
@@ -123,10 +126,12 @@ def cpu_baseline(bt, seconds):
                        f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
 
 
+VARIANTS = {}  # mode name -> workload.Variant, filled by main()
+
+
 def capture(bt, mode):
     """The whole decode step (every layer) as one HIP graph."""
     import torch
-    from paper_2609_19702_amd import workload
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         run_step(bt, mode)
@@ -135,7 +140,8 @@ def capture(bt, mode):
 
 def run_step(bt, mode, timers=None):
     from paper_2609_19702_amd import workload
-    workload.step(bt, dense=mode == "dense", fused=mode == "fused", timers=timers)
+    workload.step(bt, dense=mode == "dense", fused=mode == "fused", timers=timers,
+                  variant=VARIANTS.get(mode))
 
 
 def timed_steps(bt, steps, mode, graph):
@@ -195,11 +201,15 @@ def main():
     t0 = time.time()
     bt = workload.make_batch(w)
     workload.build_histories(bt)
+    modes = (args.only,) if args.only else ("fused", "separate", "dense", "diag_sink4", "streaming")
+    if "diag_sink4" in modes:
+        VARIANTS["diag_sink4"] = workload.make_variant(bt, "diag_sink4", B.MODE_DIAGONAL, 4)
+    if "streaming" in modes:
+        VARIANTS["streaming"] = workload.make_variant(bt, "streaming", B.MODE_WINDOW, 4)
     torch.cuda.synchronize()
     print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
           f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
 
-    modes = (args.only,) if args.only else ("fused", "separate", "dense")
     for _ in range(args.warmup):
         for mode in modes:
             run_step(bt, mode)
@@ -270,6 +280,12 @@ def main():
         "separate_calls": {
             "ms_per_step": ms["separate"], "tokens_per_s": w.batch / (ms["separate"] * 1e-3),
             "decode_launch_us": statistics.fmean(launch["separate"]) * 1e3,
+        },
+        "variants": {
+            m: {"ms_per_step": ms[m], "tokens_per_s": w.batch / (ms[m] * 1e-3),
+                "decode_launch_us": statistics.fmean(launch[m]) * 1e3,
+                "mode": "diagonal, 4 sinks" if m == "diag_sink4" else "window, 4 sinks"}
+            for m in ("diag_sink4", "streaming")
         },
         "speedup_vs_dense": ms_dense / ms_sparse,
         "ideal_speedup": bytes_dense / bytes_sparse,

@@ -711,12 +711,15 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
 }
 
 // Fused step, several splits: one workgroup per (request, KV head).  Its
-// waves merge the splits of the group's query heads (head g on wave g mod 4)
-// while the last wave also runs the phase-2 selection on the window logits
-// and the plan the split workgroups wrote (the selection does not depend on
-// the merged outputs).
+// first min(G, 4) waves merge the splits of the group's query heads while
+// one more wave runs the phase-2 selection on the window logits and the plan
+// the split workgroups wrote (the selection does not depend on the merged
+// outputs, so the two run side by side).
+constexpr int kCombineWaves = kWaves;
+
 template <int D, int G>
-__global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kBlock + 64) void combine_select_kernel(DecodeArgs a) {
+  constexpr int CW = G < kCombineWaves ? G : kCombineWaves;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int pair = blockIdx.x;
@@ -725,8 +728,10 @@ __global__ __launch_bounds__(kBlock) void combine_select_kernel(DecodeArgs a) {
   const RowRange rr = row_range<true>(a, b, pair);
   const int nsplit = (rr.n + a.C - 1) / a.C;
   if (nsplit <= 1) return;
-  for (int g = wave; g < G; g += kWaves) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
-  if (wave != kWaves - 1) return;
+  if (wave < CW) {
+    for (int g = wave; g < G; g += CW) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
+    return;
+  }
   const int t = rr.t;
   if (t < a.Natt - 1 || t > a.Nr + a.Ns - 2) return;
   const int k = t - (a.Natt - 1);
@@ -788,7 +793,8 @@ launched:
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || d.S <= 1) return e;
   if (FUSED) {
-    combine_select_kernel<D, G><<<d.B * d.Hkv, kBlock, 0, st>>>(a);
+    constexpr int cw = G < kCombineWaves ? G : kCombineWaves;
+    combine_select_kernel<D, G><<<d.B * d.Hkv, 64 * (cw + 1), 0, st>>>(a);
   } else {
     const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
     combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);

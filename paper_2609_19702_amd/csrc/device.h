@@ -92,11 +92,56 @@ __device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2)
 // group's window softmaxes.  Ties go to the smallest j (the oldest key).
 // Called by a whole wave; every lane returns the same index (or a value
 // outside [0, n) only if every score is NaN).
+//
+// Windows of up to kArgminRegs * 64 keys are read once, every load issued
+// before the first use, and kept in registers for the max, sum and score
+// passes; longer windows stream the logits once per pass.  Both forms add
+// the same terms in the same order.
+constexpr int kArgminRegs = 4;
+
 template <int G, typename Logit>
 __device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
   float best = __builtin_inff();
   int jbest = 0x7fffffff;
-  if constexpr (G == 1) {
+  if (n <= 64 * kArgminRegs) {
+    float v[G][kArgminRegs];
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c) {
+      const int j = lane + 64 * c;
+#pragma unroll
+      for (int g = 0; g < G; ++g) v[g][c] = j < n ? logit(g, j) : -__builtin_inff();
+    }
+    if constexpr (G == 1) {
+#pragma unroll
+      for (int c = 0; c < kArgminRegs; ++c)
+        if (lane + 64 * c < n) argmin_merge(best, jbest, v[0][c], lane + 64 * c);
+    } else {
+      float mx[G], inv[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float m = -__builtin_inff();
+#pragma unroll
+        for (int c = 0; c < kArgminRegs; ++c) m = fmaxf(m, v[g][c]);
+        m = wave_max(m);
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < kArgminRegs; ++c)
+          if (lane + 64 * c < n) s += __expf(v[g][c] - m);
+        s = wave_sum(s);
+        mx[g] = m;
+        inv[g] = 1.f / s;
+      }
+#pragma unroll
+      for (int c = 0; c < kArgminRegs; ++c) {
+        if (lane + 64 * c < n) {
+          float sigma = 0.f;
+#pragma unroll
+          for (int g = 0; g < G; ++g) sigma += __expf(v[g][c] - mx[g]) * inv[g];
+          argmin_merge(best, jbest, sigma, lane + 64 * c);
+        }
+      }
+    }
+  } else if constexpr (G == 1) {
     for (int j = lane; j < n; j += 64) argmin_merge(best, jbest, logit(0, j), j);
   } else {
     float mx[G], inv[G];

@@ -8,8 +8,10 @@ select pipeline over the phase-2 steps with per-step synthetic queries:
 at step ``u`` a request whose position ``t_b`` is still ahead runs at
 position ``u``, and the others are marked unused (position -1).
 
-``step`` runs one decode step (all layers) in diagonal or dense mode; every
-launch goes to the current torch stream and nothing synchronises.
+``step`` runs one decode step (all layers) in diagonal or dense mode, or in
+one of the sink variants of section 5.1 (``make_variant``: Diagonal+Sink,
+StreamingLLM) over the same KV and queries; every launch goes to the current
+torch stream and nothing synchronises.
 """
 
 from __future__ import annotations
@@ -74,21 +76,47 @@ def make_batch(w: synth.Workload, layers: Optional[int] = None, device="cuda",
     return Batch(w, p, pd, s, pos, pos_host, out, dense_bufs, 1.0 / math.sqrt(w.head_dim))
 
 
-def build_histories(bt: Batch, device="cuda"):
+@dataclass
+class Variant:
+    """Another index-builder mode over the batch's KV and queries, with its
+    own per-layer buffers."""
+    name: str
+    p: B.Params
+    bufs: List[B.Buffers]
+
+
+def build_histories(bt: Batch, device="cuda", p: Optional[B.Params] = None,
+                    bufs: Optional[List[B.Buffers]] = None):
     """Run the phase-2 steps of every layer so that each state holds the skip
-    entries appended before its request's decode position."""
-    p, s, w = bt.p, bt.s, bt.w
-    last = min(max(bt.pos_host) - 1, p.window - 2)
-    for li, L in enumerate(bt.layers):
-        B.state_reset(p, s, L.bufs.state)
+    entries appended before its request's decode position (``p``/``bufs``:
+    another mode's parameters and buffers; default the batch's own)."""
+    p = bt.p if p is None else p
+    bufs = [L.bufs for L in bt.layers] if bufs is None else bufs
+    s, w = bt.s, bt.w
+    if B.state_layout(p, s).cap == 0:
+        return  # nothing is ever selected
+    last = min(max(bt.pos_host) - 1, p.window + p.sinks - 2)
+    for li, (L, bf) in enumerate(zip(bt.layers, bufs)):
+        B.state_reset(p, s, bf.state)
         for u in range(p.n_att - 1, last + 1):
             pos = torch.tensor([u if u < t else -1 for t in bt.pos_host], dtype=torch.int32,
                                device=device)
             q = synth.step_query(w, li, u, device)
-            B.plan(p, s, pos, L.bufs.state, L.bufs.plan)
-            B.decode_attention(p, s, q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), pos, L.bufs.plan,
-                               bt.scale, L.bufs.out, L.bufs.logits, L.bufs.workspace)
-            B.select(p, s, pos, L.bufs.plan, L.bufs.logits, L.bufs.state)
+            B.plan(p, s, pos, bf.state, bf.plan)
+            B.decode_attention(p, s, q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), pos, bf.plan,
+                               bt.scale, bf.out, bf.logits, bf.workspace)
+            B.select(p, s, pos, bf.plan, bf.logits, bf.state)
+
+
+def make_variant(bt: Batch, name: str, mode: int, sinks: int, device="cuda") -> Variant:
+    """The batch's window and N_att in another mode (section 5.1 variants:
+    diagonal mode with sinks is Diagonal+Sink, window mode with sinks is
+    StreamingLLM), with its selection histories built."""
+    p = B.make_params(bt.p.prompt_len, bt.p.grid_h, bt.p.grid_w, bt.p.window, bt.p.n_att, mode,
+                      sinks)
+    v = Variant(name, p, [B.alloc_buffers(p, bt.s, device) for _ in bt.layers])
+    build_histories(bt, device, v.p, v.bufs)
+    return v
 
 
 def sparse_layer(bt: Batch, L: Layer, timer=None):
@@ -110,11 +138,22 @@ def dense_layer(bt: Batch, L: Layer, timer=None):
                        bt.scale, db.out, None, db.workspace, events=timer)
 
 
-def step(bt: Batch, dense: bool = False, timers=None, fused: bool = False):
+def variant_layer(bt: Batch, v: Variant, i: int, timer=None):
+    L, bf = bt.layers[i], v.bufs[i]
+    B.decode_step(v.p, bt.s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, bf.state, bf.plan,
+                  bt.scale, bf.out, bf.logits, bf.workspace, events=timer)
+
+
+def step(bt: Batch, dense: bool = False, timers=None, fused: bool = False,
+         variant: Optional[Variant] = None):
     """One decode step over all layers: dense mode, the three separate calls
-    (plan, decode, select) or the fused step.  ``timers[i]`` (a pair from
-    ``binding.timing_events``) receives the start and end of layer i's
-    split-K decode kernel when given."""
-    fn = dense_layer if dense else (fused_layer if fused else sparse_layer)
+    (plan, decode, select), the fused step, or the fused step of a variant.
+    ``timers[i]`` (a pair from ``binding.timing_events``) receives the start
+    and end of layer i's split-K decode kernel when given."""
     for i, L in enumerate(bt.layers):
-        fn(bt, L, None if timers is None else timers[i])
+        tm = None if timers is None else timers[i]
+        if variant is not None:
+            variant_layer(bt, variant, i, tm)
+        else:
+            fn = dense_layer if dense else (fused_layer if fused else sparse_layer)
+            fn(bt, L, tm)
