@@ -26,6 +26,9 @@ Sparse Attention", Algorithm 1 and the "Detailed explanation" paragraph):
                    per KV head, in diagonal or dense mode.
 * ``params``    -- the parameter rules of the "Parameter selection"
                    paragraph and the sparsity definition of section 5.1.
+* ``fp8``       -- exact decoding of an fp8 (OCP E4M3) KV cache with per-
+                   (request, KV head) scales, the KV quantization the paper
+                   calls orthogonal to its method (section 6).
 
 Parity status: every function is pinned in ``tests/test_oracle_*.py`` except
 the GQA aggregation of the selection weights (one skip set per KV head, score
@@ -34,4 +37,4 @@ reduction to the paper's per-head rule at group size 1 is pinned, the rest is
 "parity unpinned".
 """
 
-from . import alg1, attention, params, step  # noqa: F401
+from . import alg1, attention, fp8, params, step  # noqa: F401
