@@ -13,7 +13,8 @@ instead).  The dense mode of the
 same kernels, on the same inputs and positions, is timed alongside for the
 speedup, and so are the fused steps of the sink variants of section 5.1 at
 the same budget N_att (Diagonal+Sink4, and StreamingLLM: 4 sinks plus a
-recent window, no selection).  Prints one JSON line.
+recent window, no selection), and the fused step over an fp8 (E4M3) copy of
+the caches.  Prints one JSON line.
 
 ``roofline`` describes the decode kernel (the dominant one): algorithmic K/V
 bytes per launch (4*d bytes per attended key per KV head) divided by its
@@ -51,7 +52,7 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--only", default=None,
-                    choices=["fused", "separate", "dense", "diag_sink4", "streaming"],
+                    choices=["fused", "separate", "dense", "diag_sink4", "streaming", "fp8_kv"],
                     help="time one step variant only (shorter profiler runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                     help="run a plain device copy of MB megabytes 10 times and exit (the "
@@ -61,7 +62,7 @@ def parse():
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for name in ("decode.hip", "device.h", "internal.h"):
+    for name in ("decode.hip", "decode_fp8.hip", "decode_impl.h", "device.h", "internal.h"):
         with open(os.path.join(ROOT, "paper_2609_19702_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -201,11 +202,14 @@ def main():
     t0 = time.time()
     bt = workload.make_batch(w)
     workload.build_histories(bt)
-    modes = (args.only,) if args.only else ("fused", "separate", "dense", "diag_sink4", "streaming")
+    modes = (args.only,) if args.only else ("fused", "separate", "dense", "diag_sink4", "streaming",
+                                             "fp8_kv")
     if "diag_sink4" in modes:
         VARIANTS["diag_sink4"] = workload.make_variant(bt, "diag_sink4", B.MODE_DIAGONAL, 4)
     if "streaming" in modes:
         VARIANTS["streaming"] = workload.make_variant(bt, "streaming", B.MODE_WINDOW, 4)
+    if "fp8_kv" in modes:
+        VARIANTS["fp8_kv"] = workload.make_variant(bt, "fp8_kv", B.MODE_DIAGONAL, 0, fp8=True)
     torch.cuda.synchronize()
     print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
           f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
@@ -284,8 +288,11 @@ def main():
         "variants": {
             m: {"ms_per_step": ms[m], "tokens_per_s": w.batch / (ms[m] * 1e-3),
                 "decode_launch_us": statistics.fmean(launch[m]) * 1e3,
-                "mode": "diagonal, 4 sinks" if m == "diag_sink4" else "window, 4 sinks"}
-            for m in ("diag_sink4", "streaming")
+                "decode_launch_gbps": bt.kv_bytes(False, 1 if m == "fp8_kv" else 2) / n_layers
+                / (statistics.fmean(launch[m]) * 1e-3) / 1e9,
+                "mode": {"diag_sink4": "diagonal, 4 sinks", "streaming": "window, 4 sinks",
+                         "fp8_kv": "diagonal, fp8 E4M3 KV with per-(request, KV head) scales"}[m]}
+            for m in ("diag_sink4", "streaming", "fp8_kv")
         },
         "speedup_vs_dense": ms_dense / ms_sparse,
         "ideal_speedup": bytes_dense / bytes_sparse,

@@ -58,7 +58,7 @@ extern "C" {
 
 #define DSA_API __attribute__((visibility("default")))
 
-#define DSA_ABI_VERSION 2
+#define DSA_ABI_VERSION 3
 
 /* ---- status codes -------------------------------------------------------- */
 typedef int32_t dsa_status;
@@ -72,6 +72,11 @@ typedef int32_t dsa_status;
 #define DSA_MODE_DENSE    0 /* attend prompt + decode rows 0 .. t            */
 #define DSA_MODE_DIAGONAL 1 /* attend prompt + the rows Algorithm 1 keeps     */
 #define DSA_MODE_WINDOW   2 /* attend prompt + sinks + the most recent rows   */
+
+/* ---- KV cache element types ------------------------------------------------ */
+#define DSA_KV_BF16     0 /* IEEE bfloat16                                     */
+#define DSA_KV_FP8_E4M3 1 /* OCP 8-bit float E4M3 ("FN": no infinities,
+                             max 448) times a per-(request, KV head) scale  */
 
 /* ---- per-(request, KV head) flag bits (plan and state buffers) ------------ */
 #define DSA_FLAG_INACTIVE      1  /* decode position < 0: request slot unused   */
@@ -124,8 +129,8 @@ typedef struct dsa_shape {
 
 /*
  * Where row r of KV head h of request b lives in the K and V arrays (both
- * arrays share one layout).  Rows 0 .. L_p-1 are the prompt.  Element offset
- * of a row's first element:
+ * arrays share one layout and one element type).  Rows 0 .. L_p-1 are the
+ * prompt.  Element offset of a row's first element:
  *     base(b) + h * stride_head + r * stride_row
  * with base(b) = d_row_base[b] when d_row_base is non-NULL (a device array of
  * B int64 values, e.g. for ragged packing), else b * stride_batch.
@@ -138,11 +143,20 @@ typedef struct dsa_shape {
  * N_r + L_p) and needs R >= S + N_r; window mode needs R >= N_att; dense
  * mode reads every decode row, so a ring must hold R >= H*W there.  A ring
  * of R >= H*W rows is the linear cache.
- * A row holds head_dim contiguous bf16 values.  The K/V base pointers and
- * every base(b), stride_head and stride_row must be multiples of 8 elements
- * (16 bytes).  The caller guarantees every row the step reads exists and
- * holds the KV of the position it stands for (linear: rows up to L_p + t_b;
- * ring: the sinks and the slots of the positions the step can keep).
+ * A row holds head_dim contiguous elements of type dtype:
+ *   DSA_KV_BF16      2 bytes each; d_k_scale and d_v_scale must be NULL.
+ *   DSA_KV_FP8_E4M3  1 byte each; element value = E4M3 value of the byte
+ *                    times d_k_scale[b*Hkv + h] (K) or d_v_scale[b*Hkv + h]
+ *                    (V), fp32 device arrays of B*Hkv scales, or 1 where the
+ *                    pointer is NULL.  Bytes 0x7F and 0xFF (NaN) give
+ *                    unspecified outputs.  KV quantization is orthogonal to
+ *                    the selection (section 6): it halves the bytes per kept
+ *                    key and changes nothing else.
+ * The K/V base pointers must be 16-byte aligned, and every base(b),
+ * stride_head and stride_row must be a multiple of 8 elements.  The caller
+ * guarantees every row the step reads exists and holds the KV of the
+ * position it stands for (linear: rows up to L_p + t_b; ring: the sinks and
+ * the slots of the positions the step can keep).
  */
 typedef struct dsa_kv_layout {
   const int64_t* d_row_base;
@@ -150,6 +164,9 @@ typedef struct dsa_kv_layout {
   int64_t stride_head;
   int64_t stride_row;
   int64_t ring_rows;
+  const float* d_k_scale;
+  const float* d_v_scale;
+  int32_t dtype;
 } dsa_kv_layout;
 
 /* Byte offsets of the arrays inside a plan buffer (all int32):
@@ -279,7 +296,7 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
  * workgroups with an fp32 online softmax; a second kernel merges the chunks
  * by log-sum-exp when a request has more than one.
  *   d_q              bf16 [B][Hq][d]
- *   d_k, d_v         bf16 caches in the dsa_kv_layout layout
+ *   d_k, d_v         bf16 or fp8 caches in the dsa_kv_layout layout
  *   d_decode_pos     int32 [B] as for dsa_plan
  *   d_plan           plan of the same step (sparse modes); may be NULL in
  *                    dense mode
@@ -287,8 +304,8 @@ DSA_API dsa_status dsa_plan(const dsa_params* p, const dsa_shape* s, const int32
  *   d_out            fp32 [B][Hq][d]; zeros for unused slots
  *   d_window_logits  NULL, or fp32 [B][Hq][cap]: sm_scale * q . k of every
  *                    kept decode row in plan order, sinks included (sparse
- *                    modes; entries past count are not written).  dsa_select
- *                    reads them.
+ *                    modes; entries past count are not written; k is the
+ *                    scaled value for fp8 caches).  dsa_select reads them.
  *   d_ws, ws_bytes   workspace of at least dsa_workspace_bytes() bytes
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
  */

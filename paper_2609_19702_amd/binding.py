@@ -23,6 +23,8 @@ LIB_PATH = os.path.join(_PKG, "libdsa.so")
 MODE_DENSE = 0
 MODE_DIAGONAL = 1
 MODE_WINDOW = 2
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
 
 FLAG_INACTIVE = 1
 FLAG_POS_CLAMPED = 2
@@ -57,7 +59,8 @@ class Shape(C.Structure):
 class KVLayout(C.Structure):
     _fields_ = [("d_row_base", C.c_void_p), ("stride_batch", C.c_int64),
                 ("stride_head", C.c_int64), ("stride_row", C.c_int64),
-                ("ring_rows", C.c_int64)]
+                ("ring_rows", C.c_int64), ("d_k_scale", C.c_void_p), ("d_v_scale", C.c_void_p),
+                ("dtype", C.c_int32)]
 
 
 class PlanLayout(C.Structure):
@@ -221,15 +224,26 @@ def plan(p, s, decode_pos, state, plan_buf, stream=None):
 
 
 def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None,
-              ring_rows: int = 0) -> KVLayout:
+              ring_rows: int = 0, k_scale: Optional[torch.Tensor] = None,
+              v_scale: Optional[torch.Tensor] = None) -> KVLayout:
     """Layout of a ``[B, Hkv, rows, d]`` cache (any strides with unit stride
     along d); ``row_base`` optionally gives per-request base offsets;
     ``ring_rows = R > 0`` stores decode position ``j`` at row ``L_p + j``
-    for the ``S`` sinks and at ``L_p + S + (j - S) % (R - S)`` after them."""
+    for the ``S`` sinks and at ``L_p + S + (j - S) % (R - S)`` after them.
+    A bf16 cache is ``torch.bfloat16``; an fp8 (OCP E4M3) cache is
+    ``torch.float8_e4m3fn`` or its bytes as ``torch.uint8``, with optional
+    fp32 ``k_scale``/``v_scale`` of ``B * Hkv`` values."""
     sb, sh, sr, sd = k.stride()
     if sd != 1:
         raise ValueError("head_dim must be contiguous")
-    return KVLayout(_ptr(row_base), sb, sh, sr, int(ring_rows))
+    if k.dtype == torch.bfloat16:
+        dtype = KV_BF16
+    elif k.dtype in (torch.uint8, torch.float8_e4m3fn):
+        dtype = KV_FP8_E4M3
+    else:
+        raise ValueError(f"unsupported KV dtype {k.dtype}")
+    return KVLayout(_ptr(row_base), sb, sh, sr, int(ring_rows), _ptr(k_scale), _ptr(v_scale),
+                    dtype)
 
 
 def decode_attention(p, s, q, k, v, layout: KVLayout, decode_pos, plan_buf, sm_scale, out,

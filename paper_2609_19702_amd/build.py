@@ -5,7 +5,11 @@
 compiles every ``csrc/*.hip`` with hipcc and links them into
 ``paper_2609_19702_amd/libdsa.so``.  Packed fp32 instructions are disabled
 for device code; the host pass of hipcc prints a warning that it does not
-know that feature, which is harmless.
+know that feature, which is harmless.  Floating-point contraction is off:
+the kernels write every fused multiply-add they want as ``fmaf``, so each
+instantiation (bf16 or fp8 loads, plain or fused step, either mode) rounds
+the same expression the same way and results that should agree bit for bit
+do.
 """
 
 from __future__ import annotations
@@ -27,7 +31,7 @@ ARCH = "gfx950"
 
 CXXFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
-    "-Wall", "-Wno-unused-function",
+    "-Wall", "-Wno-unused-function", "-ffp-contract=off",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE, "-I", CSRC,
 ]

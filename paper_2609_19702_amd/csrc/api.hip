@@ -319,6 +319,9 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
     if (d.state_cap > 0 && d.Nr > dsa::kMaxFusedWindow) return DSA_ERR_UNSUPPORTED;
   }
   if (!std::isfinite(sm_scale)) return DSA_ERR_INVALID_ARG;
+  if (kv->dtype != DSA_KV_BF16 && kv->dtype != DSA_KV_FP8_E4M3) return DSA_ERR_INVALID_ARG;
+  if (kv->dtype == DSA_KV_BF16 && (kv->d_k_scale || kv->d_v_scale)) return DSA_ERR_INVALID_ARG;
+  const int64_t esz = kv->dtype == DSA_KV_BF16 ? 2 : 1;
   if (kv->stride_row < d.D || kv->stride_head < 0 || kv->stride_batch < 0)
     return DSA_ERR_INVALID_ARG;
   if ((kv->stride_row | kv->stride_head | kv->stride_batch) & 7) return DSA_ERR_INVALID_ARG;
@@ -335,12 +338,15 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
   const char* pb = static_cast<const char*>(d_plan);
   dsa::DecodeArgs a{};
   a.q = static_cast<const uint16_t*>(d_q);
-  a.k = static_cast<const uint16_t*>(d_k);
-  a.v = static_cast<const uint16_t*>(d_v);
+  a.k = static_cast<const uint8_t*>(d_k);
+  a.v = static_cast<const uint8_t*>(d_v);
   a.row_base = kv->d_row_base;
-  a.sb = kv->stride_batch;
-  a.sh = kv->stride_head;
-  a.sr = kv->stride_row;
+  a.sb = kv->stride_batch * esz;
+  a.sh = kv->stride_head * esz;
+  a.sr = kv->stride_row * esz;
+  a.ks = kv->d_k_scale;
+  a.vs = kv->d_v_scale;
+  a.kv_dtype = kv->dtype;
   a.pos = d_decode_pos;
   a.count = pb ? reinterpret_cast<const int32_t*>(pb + d.plan.count_offset) : nullptr;
   a.idx = pb ? reinterpret_cast<const int32_t*>(pb + d.plan.indices_offset) : nullptr;

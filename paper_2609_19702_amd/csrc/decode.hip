@@ -1,828 +1,19 @@
-// Split-K single-query decode attention over the prompt KV plus the kept (or,
-// in dense mode, all) decode KV; the cross-split log-sum-exp combine; and the
-// fused decode step that also builds the kept set and runs the phase-2
-// selection.
-//
-// Attn(Q_t, K_p + K[idx], V_p + V[idx]) of Algorithm 1 (section 4) for one
-// (request, KV head, split) per workgroup.  The keys of a (request, KV head)
-// are numbered r = 0 .. n-1: the L_p prompt rows, then the kept decode rows in
-// ascending position (dense mode: decode rows 0 .. t).  Split s covers keys
-// [s*C, min(n, (s+1)*C)).
-//
-// Data path (HBM-bound: each bf16 K/V element is read once and used for one
-// multiply-add per query head of the group):
-//   - a lane loads 16 bytes (8 bf16) of a row, so a 64-lane wave loads
-//     512/d rows per instruction with 128-bit coalesced accesses (one row =
-//     d/8 consecutive lanes = one contiguous 128/256-byte segment);
-//   - a wave works on tiles of U load instructions (U*512/d rows) and issues
-//     every K and V load of a tile before using any of them; rows past the
-//     end of the split read a valid row and get weight 0, so no load sits
-//     behind a branch;
-//   - tiles hold either prompt rows or kept decode rows, never both; the
-//     kept positions of a window tile are held one per lane and handed to
-//     the row groups with ds_bpermute, prompt tiles need none;
-//   - K/V rows are loaded with the non-temporal hint (streamed once);
-//   - with a ring layout a kept decode position j >= S (S sinks) is read
-//     from slot S + (j - S) mod (ring - S) (the ring holds the sinks and the
-//     live window; evicted rows are gone);
-//   - a workgroup has as many waves (1..4) as its split has tiles, so no wave
-//     sits idle holding registers;
-//   - q.k partial sums are reduced inside the row's lane group with DPP row
-//     permutations (no LDS);
-//   - softmax runs online in fp32 (base-2 exponent with the scale folded
-//     in), one running (max, sum, acc[8]) per lane and query head;
-//   - lane groups, then the waves (through LDS), are merged by log-sum-exp at
-//     the end; one split writes the final output directly, several splits
-//     write fp32 partials (acc[d], max, sum) that a second kernel merges.
-//
-// The fused step (FUSED = true, diagonal mode) reads the selection state
-// instead of a plan: each wave that owns kept decode rows rebuilds the skip
-// set of its (request, KV head) as a bitmap in its own LDS slice and ranks the
-// window positions with ballots, writing the plan as a by-product, before
-// any wave of the workgroup starts loading K/V (the workgroup then streams
-// all its rows together rather than the kept rows trailing); when one
-// split covers the whole (request, KV head) the same workgroup then runs the
-// phase-2 argmin on the window logits it computed and appends the skip entry.
-// Every value it produces is bit-identical to dsa_plan -> dsa_decode_attention
-// -> dsa_select.  The same path serves the sink variants of section 5.1: the
-// S sinks are the first S kept ranks, the window rule applies to the later
-// positions, and window mode (no stored offsets) skips the bitmap.
-#include <hip/hip_ext.h>
-
-#include "device.h"
-#include "internal.h"
+// The decode kernels for bf16 K/V caches, and the entry points that pick the
+// instantiation for a call's K/V element type.
+#include "decode_impl.h"
 
 namespace dsa {
-namespace {
-
-constexpr int kPre = 8;  // stored skip offsets per lane loaded up front
-
-// Keys of the (request, KV head) and the clamped decode position.
-struct RowRange {
-  int n;      // keys; 0 for an unused slot
-  int t;      // decode position after clamping, or -1
-  int flags;  // DSA_FLAG_INACTIVE / DSA_FLAG_POS_CLAMPED
-};
-
-template <bool FUSED>
-__device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pair) {
-  RowRange r{0, -1, 0};
-  int t = a.pos[b];
-  if (t < 0) {
-    r.flags = DSA_FLAG_INACTIVE;
-    return r;
-  }
-  if (t >= a.Ldec) {
-    t = a.Ldec - 1;
-    r.flags = DSA_FLAG_POS_CLAMPED;
-  }
-  int nwin;
-  if (a.mode == DSA_MODE_DENSE)
-    nwin = t + 1;
-  else if (FUSED)
-    nwin = min(t + 1, a.Natt);  // the kept count of Algorithm 1 at step t
-  else
-    nwin = min(max(a.count[pair], 0), a.plan_cap);
-  r.n = a.Lp + nwin;
-  r.t = t;
-  return r;
-}
-
-// Wave-private skip set of one (request, KV head) for the fused step: the
-// bitmap of the first nuse stored offsets, plus the ranking cursor.
-struct SkipSet {
-  uint32_t* bm;
-  int t, dmax;   // window offsets 0 .. dmax (dmax < 0: no window yet)
-  int sk;        // sinks kept ahead of the window: min(S, t + 1)
-  bool any;      // the bitmap holds at least one skipped offset
-  int p0, rank;  // next candidate chunk and kept positions before it
-  int flags;
-};
-
-__device__ __forceinline__ void fence_wave() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-
-// Stored count and the first kPre*64 stored offsets of a (request, KV
-// head), loaded into registers ahead of their use.
-struct StateRegs {
-  int cnt;
-  int dv[kPre];
-};
-
-__device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, StateRegs& sr) {
-  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-  sr.cnt = a.state_cap > 0 ? a.st_count[pair] : 0;
-#pragma unroll
-  for (int i = 0; i < kPre; ++i) {
-    const int e = lane + 64 * i;
-    sr.dv[i] = e < a.state_cap ? off[e] : 0;
-  }
-}
-
-__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, uint32_t* bm,
-                               const StateRegs& sr, SkipSet& ss) {
-  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-  for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
-  const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
-  int flags = sr.cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
-  const int nuse = min(max(sr.cnt, 0), nvalid);
-  fence_wave();
-  bool bad = false;
-#pragma unroll
-  for (int i = 0; i < kPre; ++i) {
-    const int e = lane + 64 * i;
-    if (e < nuse) {
-      const int d = sr.dv[i];
-      if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
-    }
-  }
-  for (int e = lane + 64 * kPre; e < nuse; e += 64) {
-    const int d = off[e];
-    if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
-  }
-  if (__ballot(bad)) flags |= DSA_FLAG_BAD_OFFSET;
-  fence_wave();
-  ss.bm = bm;
-  ss.t = t;
-  ss.sk = min(a.Ns, t + 1);
-  ss.dmax = min(t - a.Ns, a.Nr - 1);
-  ss.any = nuse > 0;
-  ss.p0 = t - ss.dmax;
-  ss.rank = ss.sk;
-  ss.flags = flags;
-}
-
-__device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
-  if (p > ss.t) return false;
-  if (!ss.any) return true;
-  const int d = ss.t - p;
-  return ((ss.bm[d >> 5] >> (d & 31)) & 1u) == 0u;
-}
-
-// Kept window positions of ranks [lo, hi) (ascending position), written to
-// kp[rank - kp_base] and to the plan.  The cursor only moves forward, so the
-// tiles of a wave (in increasing rank order) share one scan.
-__device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss, int lo, int hi,
-                            int* kp, int kp_base) {
-  const uint64_t below = (uint64_t(1) << lane) - 1;
-  int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
-  for (int r = lo + lane; r < min(hi, ss.sk); r += 64) {  // sink rank r is position r
-    kp[r - kp_base] = r;
-    plan[r] = r;
-  }
-  while (ss.p0 <= ss.t && ss.rank < hi) {
-    const int p = ss.p0 + lane;
-    const bool kept = is_kept(ss, p);
-    const uint64_t mask = __ballot(kept);
-    const int rk = ss.rank + __popcll(mask & below);
-    if (kept && rk >= lo && rk < hi) {
-      kp[rk - kp_base] = p;
-      plan[rk] = p;
-    }
-    const int tot = ss.rank + __popcll(mask);
-    if (tot > hi) break;  // the chunk reaches past this tile: keep it for the next one
-    ss.rank = tot;
-    ss.p0 += 64;
-  }
-  fence_wave();
-}
-
-// Total kept positions of the window (for the DSA_FLAG_COUNT check).
-__device__ int count_kept(const SkipSet& ss, int lane) {
-  int n = ss.sk;
-  for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64) n += __popcll(__ballot(is_kept(ss, p0 + lane)));
-  return n;
-}
-
-// One 32-row tile of the grouped-head path.  q.K^T runs on
-// v_mfma_f32_16x16x32_bf16: K rows are loaded straight into the A layout
-// (lane l: row l%16, 8 elements per k-step), the group's queries are the B
-// operand, and the C layout leaves head l%16's scores of rows 4*(l/16)+j in
-// lane l.  The softmax statistics stay in that layout; the weights reach the
-// V-layout lanes through a small LDS slice of the wave, and P.V runs in fp32
-// on the vector ALUs (bf16 weights would cost ~2^-9 relative error).
-template <int D, int G, bool FUSED>
-__device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs, int re,
-                                          bool has_win, int pos_l, const uint16_t* kmf,
-                                          const uint16_t* vb, const bf16x8* qb, int b, int kvh,
-                                          int w0, float& m_c, float& l_c, float (&acc)[G][8],
-                                          float* wls, float* ps, float* als) {
-  constexpr int LPR = D / 8, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
-  constexpr int NH = T / 16;  // 16-row MFMA blocks per tile
-  const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR;
-  uint4 kr[NH][NK];
-#pragma unroll
-  for (int h = 0; h < NH; ++h) {
-    const int r = rs + 16 * h + lr;
-    const int wpos = has_win ? __shfl(pos_l, 16 * h + lr, 64) : 0;
-    int cr = 0;  // rows past the tile end read row 0 and get weight 0
-    if (r < re) cr = has_win ? a.Lp + wpos : r;
-#pragma unroll
-    for (int i = 0; i < NK; ++i) kr[h][i] = load_stream16(kmf + cr * a.sr + 32 * i);
-  }
-  uint4 vr[UV];
-#pragma unroll
-  for (int u = 0; u < UV; ++u) {
-    const int r = rs + u * RPI + rg;
-    const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
-    int cr = 0;
-    if (r < re) cr = has_win ? a.Lp + wpos : r;
-    vr[u] = load_stream16(vb + cr * a.sr);
-  }
-  f32x4 sc[NH];
-#pragma unroll
-  for (int h = 0; h < NH; ++h) {
-    sc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < NK; ++i)
-      sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[h][i]), qb[i],
-                                                      sc[h], 0, 0, 0);
-  }
-  if (has_win && lr < G) {
-#pragma unroll
-    for (int h = 0; h < NH; ++h)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = rs + 16 * h + 4 * lq + j;
-        if (r < re) {
-          const float logit = sc[h][j] * a.scale;
-          if (a.wlog)
-            a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + lr) * a.plan_cap + (r - a.Lp)] =
-                logit;
-          if constexpr (FUSED) wls[lr * kMaxFusedSplit + (r - a.Lp - w0)] = logit;
-        }
-      }
-  }
-  float s2[NH][4];
-  float mx = kNegBig;
-#pragma unroll
-  for (int h = 0; h < NH; ++h)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      s2[h][j] = rs + 16 * h + 4 * lq + j < re ? sc[h][j] * a.scale_log2 : kNegBig;
-      mx = fmaxf(mx, s2[h][j]);
-    }
-  mx = fmaxf(mx, shfl_xor(mx, 16));
-  mx = fmaxf(mx, shfl_xor(mx, 32));
-  const float mnew = fmaxf(m_c, mx);
-  const float alpha = fast_exp2(m_c - mnew);
-  m_c = mnew;
-  l_c *= alpha;
-#pragma unroll
-  for (int h = 0; h < NH; ++h)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int rl = 16 * h + 4 * lq + j;
-      const float p = rs + rl < re ? fast_exp2(s2[h][j] - mnew) : 0.f;
-      l_c += p;
-      if (lr < G) ps[rl * G + lr] = p;
-    }
-  if (lr < G && lq == 0) als[lr] = alpha;
-  fence_wave();
-  float al[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) al[g] = als[g];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] *= al[g];
-#pragma unroll
-  for (int u = 0; u < UV; ++u) {
-    float vf[8];
-    unpack8(vr[u], vf);
-    const int rl = u * RPI + rg;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = ps[rl * G + g];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
-    }
-  }
-  fence_wave();  // the next tile rewrites ps / als
-}
-
-template <int D, int G, int U, bool FUSED, bool MF>
-__device__ __forceinline__ void decode_body(const DecodeArgs& a) {
-  constexpr int LPR = D / 8;       // lanes per row (V layout; K layout too without MF)
-  constexpr int RPI = 64 / LPR;    // rows per load instruction
-  constexpr int T = MF ? kMfmaTile : RPI * U;  // rows per wave tile (<= 64)
-  constexpr int UV = T / RPI;      // V load instructions per tile
-  constexpr int NK = D / 32;       // MFMA k-steps per 16 rows (MF only)
-  static_assert(T <= 64, "one kept position per lane");
-  static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
-  constexpr int KS = FUSED ? kMaxFusedSplit : 1;
-  constexpr int PS = MF ? kWaves : 1;
-  __shared__ float red[kWaves][G][D + 2];
-  __shared__ float wl_s[G][KS];    // fused: window logits of the split
-  __shared__ int kp_s[KS];         // fused: kept positions of the split
-  __shared__ float p_s[PS][MF ? kMfmaTile : 1][G];  // MF: softmax weights, C -> V layout
-  __shared__ float alpha_s[PS][G];                  // MF: rescale factors of the tile
-  extern __shared__ uint32_t bm_all[];  // fused: one skip bitmap per wave
-
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
-  const int rg = lane / LPR;       // row group within the wave
-  const int c = lane % LPR;        // 8-element column chunk
-  const int s = blockIdx.x % a.S;
-  const int pair = blockIdx.x / a.S;
-  const int kvh = pair % a.Hkv;
-  const int b = pair / a.Hkv;
-
-  const RowRange rr = row_range<FUSED>(a, b, pair);
-  const int n = rr.n;
-  const int r0 = s * a.C;
-  if (s > 0 && r0 >= n) return;
-  const int r1 = min(n, r0 + a.C);
-  const int nsplit = (n + a.C - 1) / a.C;
-  const bool dense = a.mode == DSA_MODE_DENSE;
-  const int w0 = max(r0, a.Lp) - a.Lp;  // first window rank of the split
-
-  const int64_t base = (a.row_base ? a.row_base[b] : static_cast<int64_t>(b) * a.sb) +
-                       static_cast<int64_t>(kvh) * a.sh + c * 8;
-  const uint16_t* kb = a.k + base;
-  const uint16_t* vb = a.v + base;
-  const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
-
-  uint4 qr[MF ? 1 : G];
-  if constexpr (!MF) {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      qr[g] = *reinterpret_cast<const uint4*>(
-          a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
-  }
-  // MFMA operands: K in the A layout (lane l: row l%16, elements
-  // 8*(l/16) + 32*i .. +7 of k-step i), q^T in the B layout (lane l: query
-  // head l%16 of the group, same elements; zero for l%16 >= G).
-  const int lr = lane & 15, lq = lane >> 4;
-  const uint16_t* kmf = a.k + (base - c * 8) + 8 * lq;
-  bf16x8 qb[MF ? NK : 1];
-  if constexpr (MF) {
-#pragma unroll
-    for (int i = 0; i < NK; ++i) {
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (lr < G)
-        x = *reinterpret_cast<const uint4*>(
-            a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + lr) * D + 32 * i + 8 * lq);
-      qb[i] = __builtin_bit_cast(bf16x8, x);
-    }
-  }
-
-  // Tiles never straddle the prompt/decode boundary: the split's prompt rows
-  // [r0, pe) and decode rows [wst, r1) are each cut into tiles of T rows,
-  // tile j going to wave j % nwaves.  Prompt tiles and dense-mode decode
-  // tiles load at once; diagonal-mode decode tiles wait for their kept
-  // positions.  (Both modes cut the same way, so with nothing skipped they
-  // add the same numbers in the same order.)
-  const int pe = min(r1, a.Lp);
-  const int wst = max(r0, a.Lp);
-  const int P = pe > r0 ? (pe - r0 + T - 1) / T : 0;
-  const int Wn = r1 > wst ? (r1 - wst + T - 1) / T : 0;
-
-  SkipSet ss{};
-  StateRegs sreg{};
-  bool have_set = false;
-  // The wave holding window rank 0 (the first decode tile of the pair)
-  // reports the plan's count and flags, as dsa_plan would.
-  bool reporter = false;
-  int rep_flags = 0;
-  if constexpr (FUSED) {
-    // First window tile of this wave, if it has one.
-    const int j0 = P + ((wave - P) % nwaves + nwaves) % nwaves;
-    if (j0 < P + Wn) load_state(a, pair, lane, sreg);
-    reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && j0 == P);
-  }
-
-  if constexpr (FUSED) {
-    // Rank every kept window row this wave owns before any wave of the
-    // workgroup loads K/V: the whole workgroup then streams its rows
-    // together instead of the window rows queueing behind the prompt rows.
-    for (int j = wave; j < P + Wn; j += nwaves) {
-      if (j < P) continue;
-      const int rs = wst + (j - P) * T;
-      const int re = min(rs + T, r1);
-      if (!have_set) {
-        build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
-        have_set = true;
-      }
-      rank_window(a, pair, lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
-    }
-    // The reporting wave settles the plan flags now, so the skip set is not
-    // live through the K/V loop.
-    if (reporter) {
-      rep_flags = rr.flags;
-      if (rr.t >= 0) {
-        rep_flags |= ss.flags;
-        const int kept = count_kept(ss, lane);
-        if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
-            kept != min(rr.t + 1, a.Natt))
-          rep_flags |= DSA_FLAG_COUNT;
-      }
-    }
-    if (Wn > 0) __syncthreads();
-  }
-
-  float qf[MF ? 1 : G][8];
-  float m[G], l[G], acc[G][8];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    if constexpr (!MF) unpack8(qr[g], qf[g]);
-    m[g] = kNegBig;
-    l[g] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
-  }
-  float m_c = kNegBig, l_c = 0.f;  // MF: running max / partial sum of head lr
-
-  for (int j = wave; j < P + Wn; j += nwaves) {
-    const bool dec = j >= P;
-    const bool has_win = dec && !dense;
-    const int rs = dec ? wst + (j - P) * T : r0 + j * T;
-    const int re = min(rs + T, dec ? r1 : pe);
-    // Kept positions of a window tile: lane i holds row rs + i.
-    int pos_l = 0;
-    if (has_win) {
-      if constexpr (FUSED) {
-        if (lane < re - rs) pos_l = kp_s[rs + lane - a.Lp - w0];
-      } else {
-        if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
-      }
-      if (a.ring && pos_l >= a.Ns) pos_l = a.Ns + (pos_l - a.Ns) % a.ring;  // ring slot
-    }
-    if constexpr (MF) {
-      mfma_tile<D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, m_c, l_c,
-                             acc, &wl_s[0][0], &p_s[wave][0][0], &alpha_s[wave][0]);
-      continue;
-    }
-    uint4 kr[U], vr[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = rs + u * RPI + rg;
-      const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
-      int cr = 0;  // rows past the tile end read row 0 and get weight 0
-      if (r < re) cr = has_win ? a.Lp + wpos : r;
-      kr[u] = load_stream16(kb + cr * a.sr);
-      vr[u] = load_stream16(vb + cr * a.sr);
-    }
-
-    float sc[U][G];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float kf[8];
-      unpack8(kr[u], kf);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float x = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x = fmaf(qf[g][e], kf[e], x);
-        sc[u][g] = group_sum<LPR>(x);
-      }
-    }
-    if (has_win && c == 0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int r = rs + u * RPI + rg;
-        if (r < re) {
-#pragma unroll
-          for (int g = 0; g < G; ++g) {
-            const float logit = sc[u][g] * a.scale;
-            if (a.wlog)
-              a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (r - a.Lp)] =
-                  logit;
-            if constexpr (FUSED) wl_s[g][r - a.Lp - w0] = logit;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float mx = kNegBig;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        sc[u][g] = rs + u * RPI + rg < re ? sc[u][g] * a.scale_log2 : kNegBig;
-        mx = fmaxf(mx, sc[u][g]);
-      }
-      const float mnew = fmaxf(m[g], mx);
-      const float alpha = fast_exp2(m[g] - mnew);
-      m[g] = mnew;
-      l[g] *= alpha;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] *= alpha;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float vf[8];
-      unpack8(vr[u], vf);
-      const bool ok = rs + u * RPI + rg < re;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float p = ok ? fast_exp2(sc[u][g] - m[g]) : 0.f;
-        l[g] += p;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
-      }
-    }
-  }
-
-  if constexpr (FUSED) {
-    if (reporter && lane == 0) {
-      a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
-      a.plan_flags[pair] = rep_flags;
-    }
-  }
-
-  if constexpr (MF) {
-    // Head g's running max sits in the lanes with lr == g; its sum is split
-    // over the four lanes lr + 16*q.  The V-layout accumulators of all row
-    // groups share that max, so they merge by plain addition.
-    float lt = l_c + shfl_xor(l_c, 16);
-    lt += shfl_xor(lt, 32);
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      m[g] = __shfl(m_c, g, 64);
-      l[g] = __shfl(lt, g, 64);
-#pragma unroll
-      for (int off = LPR; off < 64; off <<= 1)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[g][e] += shfl_xor(acc[g][e], off);
-    }
-  }
-  // Merge the row groups of the wave (lanes c, c + LPR, c + 2*LPR, ...).
-#pragma unroll
-  for (int off = LPR; off < 64 && !MF; off <<= 1) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float m2 = shfl_xor(m[g], off);
-      const float l2 = shfl_xor(l[g], off);
-      const float mn = fmaxf(m[g], m2);
-      const float a1 = fast_exp2(m[g] - mn);
-      const float a2 = fast_exp2(m2 - mn);
-      l[g] = l[g] * a1 + l2 * a2;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x2 = shfl_xor(acc[g][e], off);
-        acc[g][e] = acc[g][e] * a1 + x2 * a2;
-      }
-      m[g] = mn;
-    }
-  }
-  if (rg == 0) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) red[wave][g][c * 8 + e] = acc[g][e];
-      if (c == 0) {
-        red[wave][g][D] = m[g];
-        red[wave][g][D + 1] = l[g];
-      }
-    }
-  }
-  __syncthreads();
-
-  if constexpr (FUSED) {
-    // Phase-2 selection, when this workgroup saw every kept window key.
-    // The sinks (the first Ns kept ranks) are never candidates.
-    if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr + a.Ns - 2) {
-      const int k = rr.t - (a.Natt - 1);
-      if (k < a.state_cap) {
-        const int cnt = a.st_count[pair];
-        if (cnt < k) {
-          if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
-        } else {
-          const int nwin = n - a.Lp - a.Ns;
-          const int ns = a.Ns;
-          int jbest =
-              window_argmin<G>(lane, nwin, [&](int g, int j) { return wl_s[g][ns + j]; });
-          if (lane == 0) {
-            if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-            const int d = min(max(rr.t - kp_s[ns + jbest], 0), a.Nr - 2);
-            a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
-            a.st_count[pair] = k + 1;
-          }
-        }
-      }
-    }
-  }
-  if (wave != 0) return;
-
-  // Merge the waves; lane j handles columns j and j + 64.
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float M = kNegBig;
-    for (int w = 0; w < nwaves; ++w) M = fmaxf(M, red[w][g][D]);
-    float L = 0.f, A0 = 0.f, A1 = 0.f;
-    for (int w = 0; w < nwaves; ++w) {
-      const float sw = fast_exp2(red[w][g][D] - M);
-      L += red[w][g][D + 1] * sw;
-      A0 += red[w][g][lane] * sw;
-      if constexpr (D == 128) A1 += red[w][g][lane + 64] * sw;
-    }
-    const int h = kvh * G + g;
-    if (nsplit <= 1) {
-      const float inv = L > 0.f ? 1.f / L : 0.f;
-      float* o = a.out + (static_cast<size_t>(b) * a.Hq + h) * D;
-      o[lane] = A0 * inv;
-      if constexpr (D == 128) o[lane + 64] = A1 * inv;
-    } else {
-      float* pp = a.part + ((static_cast<size_t>(pair) * a.S + s) * G + g) * (D + 2);
-      pp[lane] = A0;
-      if constexpr (D == 128) pp[lane + 64] = A1;
-      if (lane == 0) {
-        pp[D] = M;
-        pp[D + 1] = L;
-      }
-    }
-  }
-}
-
-template <int D, int G, int U, bool FUSED>
-__global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
-  decode_body<D, G, U, FUSED, false>(a);
-}
-
-// The grouped-head (MFMA) tile holds K and V of 32 rows plus G accumulator
-// sets; the occupancy floor keeps three waves per SIMD resident (two for
-// groups of eight, whose accumulators alone take 64 registers).
-template <int D, int G, bool FUSED>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : 3, 8)))
-void decode_mfma_kernel(DecodeArgs a) {
-  decode_body<D, G, 2, FUSED, true>(a);
-}
-
-// out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s over the splits of
-// (request b, query head g of KV head kvh), in base-2 exponents (the partial
-// maxima are kept in log2 units).  Called by one wave.
-template <int D>
-__device__ __forceinline__ void combine_one(const DecodeArgs& a, int lane, int b, int kvh, int g,
-                                            int G, int nsplit) {
-  const int pair = b * a.Hkv + kvh;
-  const float* pp = a.part + (static_cast<size_t>(pair) * a.S * G + g) * (D + 2);
-  const size_t sstride = static_cast<size_t>(G) * (D + 2);
-  // Maxima and sums: one split per lane.
-  float M = kNegBig;
-  for (int s = lane; s < nsplit; s += 64) M = fmaxf(M, pp[s * sstride + D]);
-  M = wave_max(M);
-  float L = 0.f;
-  for (int s = lane; s < nsplit; s += 64)
-    L += pp[s * sstride + D + 1] * fast_exp2(pp[s * sstride + D] - M);
-  L = wave_sum(L);
-  // Weighted rows: lanes over columns, eight splits' loads in flight.
-  float A0 = 0.f, A1 = 0.f;
-  for (int s0 = 0; s0 < nsplit; s0 += 64) {
-    const int sl = s0 + lane;
-    const float w = sl < nsplit ? fast_exp2(pp[sl * sstride + D] - M) : 0.f;
-    const int n = min(64, nsplit - s0);
-    for (int j0 = 0; j0 < n; j0 += 8) {
-      float x0[8], x1[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int sj = s0 + min(j0 + j, n - 1);
-        x0[j] = pp[sj * sstride + lane];
-        if constexpr (D == 128) x1[j] = pp[sj * sstride + lane + 64];
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float sw = j0 + j < n ? __shfl(w, j0 + j, 64) : 0.f;
-        A0 = fmaf(x0[j], sw, A0);
-        if constexpr (D == 128) A1 = fmaf(x1[j], sw, A1);
-      }
-    }
-  }
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  float* o = a.out + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D;
-  o[lane] = A0 * inv;
-  if constexpr (D == 128) o[lane + 64] = A1 * inv;
-}
-
-// One wave per (request, query head).
-template <int D>
-__global__ __launch_bounds__(kBlock) void combine_kernel(DecodeArgs a, int G) {
-  const int lane = threadIdx.x & 63;
-  const int bh = blockIdx.x * kWaves + (threadIdx.x >> 6);
-  if (bh >= a.B * a.Hq) return;
-  const int b = bh / a.Hq;
-  const int h = bh % a.Hq;
-  const RowRange rr = row_range<false>(a, b, b * a.Hkv + h / G);
-  const int nsplit = (rr.n + a.C - 1) / a.C;
-  if (nsplit <= 1) return;
-  combine_one<D>(a, lane, b, h / G, h % G, G, nsplit);
-}
-
-// Fused step, several splits: one workgroup per (request, KV head).  Its
-// first min(G, 4) waves merge the splits of the group's query heads while
-// one more wave runs the phase-2 selection on the window logits and the plan
-// the split workgroups wrote (the selection does not depend on the merged
-// outputs, so the two run side by side).
-constexpr int kCombineWaves = kWaves;
-
-template <int D, int G>
-__global__ __launch_bounds__(kBlock + 64) void combine_select_kernel(DecodeArgs a) {
-  constexpr int CW = G < kCombineWaves ? G : kCombineWaves;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int pair = blockIdx.x;
-  const int b = pair / a.Hkv;
-  const int kvh = pair % a.Hkv;
-  const RowRange rr = row_range<true>(a, b, pair);
-  const int nsplit = (rr.n + a.C - 1) / a.C;
-  if (nsplit <= 1) return;
-  if (wave < CW) {
-    for (int g = wave; g < G; g += CW) combine_one<D>(a, lane, b, kvh, g, G, nsplit);
-    return;
-  }
-  const int t = rr.t;
-  if (t < a.Natt - 1 || t > a.Nr + a.Ns - 2) return;
-  const int k = t - (a.Natt - 1);
-  if (k >= a.state_cap) return;
-  const int cnt = a.st_count[pair];
-  if (cnt < k) {
-    if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
-    return;
-  }
-  const int nwin = rr.n - a.Lp - a.Ns;  // window keys after the sinks
-  const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap + a.Ns;
-  const int plan_cap = a.plan_cap;
-  int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl[g * plan_cap + j]; });
-  if (lane == 0) {
-    if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-    const int pos = a.plan_idx[static_cast<size_t>(pair) * a.plan_cap + a.Ns + jbest];
-    const int d = min(max(t - pos, 0), a.Nr - 2);
-    a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
-    a.st_count[pair] = k + 1;
-  }
-}
-
-template <int D, int G, int U, bool FUSED, bool MF>
-void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
-                  hipEvent_t t1) {
-  const int grid = d.B * d.Hkv * d.S;
-  const int block = 64 * d.NW;
-  const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * d.NW * a.words) : 0u;
-  if constexpr (MF) {
-    if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_mfma_kernel<D, G, FUSED>, dim3(grid), dim3(block), lds, st, t0,
-                            t1, 0, a);
-    else
-      decode_mfma_kernel<D, G, FUSED><<<grid, block, lds, st>>>(a);
-  } else {
-    if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_kernel<D, G, U, FUSED>, dim3(grid), dim3(block), lds, st, t0, t1,
-                            0, a);
-    else
-      decode_kernel<D, G, U, FUSED><<<grid, block, lds, st>>>(a);
-  }
-}
-
-template <int D, int G, bool FUSED>
-hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
-                     hipEvent_t t1) {
-  if constexpr (G >= 2) {
-    if (d.MF) {
-      launch_split<D, G, 2, FUSED, true>(d, a, st, t0, t1);
-      goto launched;
-    }
-  }
-  switch (d.U) {
-    case 8: launch_split<D, G, 8, FUSED, false>(d, a, st, t0, t1); break;
-    case 4: launch_split<D, G, 4, FUSED, false>(d, a, st, t0, t1); break;
-    default: launch_split<D, G, 2, FUSED, false>(d, a, st, t0, t1); break;
-  }
-launched:
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || d.S <= 1) return e;
-  if (FUSED) {
-    constexpr int cw = G < kCombineWaves ? G : kCombineWaves;
-    combine_select_kernel<D, G><<<d.B * d.Hkv, 64 * (cw + 1), 0, st>>>(a);
-  } else {
-    const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
-    combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
-  }
-  return hipGetLastError();
-}
-
-template <int D, bool FUSED>
-hipError_t launch_d(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
-                    hipEvent_t t1) {
-  switch (d.G) {
-    case 1: return launch_dg<D, 1, FUSED>(d, a, st, t0, t1);
-    case 2: return launch_dg<D, 2, FUSED>(d, a, st, t0, t1);
-    case 4: return launch_dg<D, 4, FUSED>(d, a, st, t0, t1);
-    default: return launch_dg<D, 8, FUSED>(d, a, st, t0, t1);
-  }
-}
-
-}  // namespace
 
 hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                          hipEvent_t t1) {
-  return d.D == 64 ? launch_d<64, false>(d, a, st, t0, t1) : launch_d<128, false>(d, a, st, t0, t1);
+  if (a.kv_dtype == DSA_KV_FP8_E4M3) return launch_kv_fp8(d, a, st, t0, t1, false);
+  return launch_kv<KvBf16>(d, a, st, t0, t1, false);
 }
 
 hipError_t launch_step(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                        hipEvent_t t1) {
-  return d.D == 64 ? launch_d<64, true>(d, a, st, t0, t1) : launch_d<128, true>(d, a, st, t0, t1);
+  if (a.kv_dtype == DSA_KV_FP8_E4M3) return launch_kv_fp8(d, a, st, t0, t1, true);
+  return launch_kv<KvBf16>(d, a, st, t0, t1, true);
 }
 
 }  // namespace dsa

@@ -33,6 +33,13 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
   return make_uint4(x.x, x.y, x.z, x.w);
 }
 
+// 8-byte form of the same (8 fp8 elements of a row).
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint2 load_stream8(const void* p) {
+  const u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+  return make_uint2(x.x, x.y);
+}
+
 // DPP lane permutations inside a 16-lane row.
 constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]: lane ^ 1
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]: lane ^ 2

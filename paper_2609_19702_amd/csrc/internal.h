@@ -52,10 +52,13 @@ struct PlanArgs {
 
 struct DecodeArgs {
   const uint16_t* q;
-  const uint16_t* k;
-  const uint16_t* v;
-  const int64_t* row_base;
-  int64_t sb, sh, sr;
+  const uint8_t* k;      // K/V caches, addressed in bytes
+  const uint8_t* v;
+  const int64_t* row_base;  // per-request base offsets in elements, or nullptr
+  int64_t sb, sh, sr;       // strides in bytes
+  const float* ks;          // fp8: per-(request, KV head) K / V scales, or nullptr
+  const float* vs;
+  int kv_dtype;             // DSA_KV_BF16 or DSA_KV_FP8_E4M3
   const int32_t* pos;
   const int32_t* count;  // plan counts (diagonal mode)
   const int32_t* idx;    // plan indices (diagonal mode)
@@ -100,6 +103,9 @@ hipError_t launch_decode(const Derived& d, const DecodeArgs& a, hipStream_t st,
                          hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 hipError_t launch_step(const Derived& d, const DecodeArgs& a, hipStream_t st,
                        hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+// The fp8 instantiations (their own translation unit); fused selects the step.
+hipError_t launch_kv_fp8(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
+                         hipEvent_t t1, bool fused);
 hipError_t launch_select(const Derived& d, const SelectArgs& a, hipStream_t st);
 hipError_t launch_reset(const Derived& d, const ResetArgs& a, hipStream_t st);
 

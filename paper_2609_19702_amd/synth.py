@@ -24,6 +24,13 @@ benchmark items are used):
 Values are N(0, 1) in fp32, rounded to bf16 (round to nearest even) before
 either side sees them.  Decode positions are "ragged": each request's newest
 decode position is drawn uniformly from ``[0, H*W)``.
+
+fp8 caches (``to_fp8``) are the bf16 cache stored as OCP E4M3 bytes with
+one fp32 scale per (request, KV head) for K and one for V: the largest
+magnitude of that head's rows maps to 448, and every value is rounded to
+the nearest E4M3 value by torch's float8_e4m3fn conversion.  That is how
+the test inputs are made; the library and the oracle only read the bytes
+and the scales.
 """
 
 from __future__ import annotations
@@ -121,11 +128,14 @@ def random_ints(w: Workload, layer: int, n: int, sub: int = 0) -> torch.Tensor:
 @dataclass
 class LayerKV:
     """A head-major KV cache of one layer: ``k``/``v`` are
-    ``[B, Hkv, rows, d]`` bf16 with the ``prompt_len`` prompt rows first and
-    decode position ``j`` at row ``prompt_len + j``."""
+    ``[B, Hkv, rows, d]`` bf16 (or E4M3 bytes as uint8, with fp32 scales
+    ``k_scale``/``v_scale`` of ``B * Hkv`` values) with the ``prompt_len``
+    prompt rows first and decode position ``j`` at row ``prompt_len + j``."""
     k: torch.Tensor
     v: torch.Tensor
     rows: int
+    k_scale: Optional[torch.Tensor] = None
+    v_scale: Optional[torch.Tensor] = None
 
     @property
     def strides(self):
@@ -155,6 +165,33 @@ def layer_kv(w: Workload, layer: int, device="cpu", decode_rows: Optional[int] =
         out.append(x.to(torch.bfloat16))
         del x
     return LayerKV(out[0], out[1], rows)
+
+
+E4M3_MAX = 448.0
+
+
+def _fp8_one(x: torch.Tensor):
+    """E4M3 bytes and per-(request, head) scales of a ``[B, H, rows, d]``
+    bf16 tensor, one request at a time (bounded temporary memory)."""
+    B, H = x.shape[:2]
+    codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    scale = torch.empty((B, H), dtype=torch.float32, device=x.device)
+    for b in range(B):
+        xb = x[b].float()
+        amax = xb.abs().amax(dim=(1, 2)).clamp_min(1e-30)
+        sc = amax / E4M3_MAX
+        codes[b] = (xb / sc[:, None, None]).clamp(-E4M3_MAX, E4M3_MAX).to(
+            torch.float8_e4m3fn).view(torch.uint8)
+        scale[b] = sc
+        del xb
+    return codes, scale.reshape(-1).contiguous()
+
+
+def to_fp8(kv: LayerKV) -> LayerKV:
+    """The same cache as E4M3 bytes plus per-(request, KV head) scales."""
+    kc, ks = _fp8_one(kv.k)
+    vc, vs = _fp8_one(kv.v)
+    return LayerKV(kc, vc, kv.rows, ks, vs)
 
 
 def layer_query(w: Workload, layer: int, device="cpu") -> torch.Tensor:

@@ -45,16 +45,17 @@ class Batch:
     dense_bufs: B.Buffers
     scale: float
 
-    def kv_bytes(self, dense: bool) -> int:
-        """Algorithmic K+V bytes one step streams over all layers: 4*d bytes
-        (a bf16 K row and V row) per attended key per KV head."""
+    def kv_bytes(self, dense: bool, elem_bytes: int = 2) -> int:
+        """Algorithmic K+V bytes one step streams over all layers: a K row
+        and a V row (4*d bytes in bf16, 2*d in fp8) per attended key per KV
+        head."""
         n_att = self.p.n_att
         rows = 0
         for t in self.pos_host:
             if t < 0:
                 continue
             rows += self.w.prompt_len + (t + 1 if dense else min(t + 1, n_att))
-        return rows * self.s.num_kv_heads * 4 * self.s.head_dim * len(self.layers)
+        return rows * self.s.num_kv_heads * 2 * elem_bytes * self.s.head_dim * len(self.layers)
 
 
 def make_batch(w: synth.Workload, layers: Optional[int] = None, device="cuda",
@@ -78,44 +79,56 @@ def make_batch(w: synth.Workload, layers: Optional[int] = None, device="cuda",
 
 @dataclass
 class Variant:
-    """Another index-builder mode over the batch's KV and queries, with its
-    own per-layer buffers."""
+    """Another index-builder mode, or another KV element type, over the
+    batch's queries, with its own per-layer buffers (and caches, for fp8)."""
     name: str
     p: B.Params
     bufs: List[B.Buffers]
+    kvs: Optional[List[synth.LayerKV]] = None
+
+
+def kv_layout_of(kv: synth.LayerKV) -> B.KVLayout:
+    return B.kv_layout(kv.k, k_scale=kv.k_scale, v_scale=kv.v_scale)
 
 
 def build_histories(bt: Batch, device="cuda", p: Optional[B.Params] = None,
-                    bufs: Optional[List[B.Buffers]] = None):
+                    bufs: Optional[List[B.Buffers]] = None,
+                    kvs: Optional[List[synth.LayerKV]] = None):
     """Run the phase-2 steps of every layer so that each state holds the skip
-    entries appended before its request's decode position (``p``/``bufs``:
-    another mode's parameters and buffers; default the batch's own)."""
+    entries appended before its request's decode position (``p``/``bufs``/
+    ``kvs``: another variant's parameters, buffers and caches; default the
+    batch's own)."""
     p = bt.p if p is None else p
     bufs = [L.bufs for L in bt.layers] if bufs is None else bufs
+    kvs = [L.kv for L in bt.layers] if kvs is None else kvs
     s, w = bt.s, bt.w
     if B.state_layout(p, s).cap == 0:
         return  # nothing is ever selected
     last = min(max(bt.pos_host) - 1, p.window + p.sinks - 2)
-    for li, (L, bf) in enumerate(zip(bt.layers, bufs)):
+    for li, (kv, bf) in enumerate(zip(kvs, bufs)):
         B.state_reset(p, s, bf.state)
+        lay = kv_layout_of(kv)
         for u in range(p.n_att - 1, last + 1):
             pos = torch.tensor([u if u < t else -1 for t in bt.pos_host], dtype=torch.int32,
                                device=device)
             q = synth.step_query(w, li, u, device)
             B.plan(p, s, pos, bf.state, bf.plan)
-            B.decode_attention(p, s, q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), pos, bf.plan,
-                               bt.scale, bf.out, bf.logits, bf.workspace)
+            B.decode_attention(p, s, q, kv.k, kv.v, lay, pos, bf.plan, bt.scale, bf.out, bf.logits,
+                               bf.workspace)
             B.select(p, s, pos, bf.plan, bf.logits, bf.state)
 
 
-def make_variant(bt: Batch, name: str, mode: int, sinks: int, device="cuda") -> Variant:
+def make_variant(bt: Batch, name: str, mode: int, sinks: int, device="cuda",
+                 fp8: bool = False) -> Variant:
     """The batch's window and N_att in another mode (section 5.1 variants:
     diagonal mode with sinks is Diagonal+Sink, window mode with sinks is
-    StreamingLLM), with its selection histories built."""
+    StreamingLLM), or over an fp8 copy of the caches, with its selection
+    histories built."""
     p = B.make_params(bt.p.prompt_len, bt.p.grid_h, bt.p.grid_w, bt.p.window, bt.p.n_att, mode,
                       sinks)
-    v = Variant(name, p, [B.alloc_buffers(p, bt.s, device) for _ in bt.layers])
-    build_histories(bt, device, v.p, v.bufs)
+    kvs = [synth.to_fp8(L.kv) for L in bt.layers] if fp8 else None
+    v = Variant(name, p, [B.alloc_buffers(p, bt.s, device) for _ in bt.layers], kvs)
+    build_histories(bt, device, v.p, v.bufs, v.kvs)
     return v
 
 
@@ -140,7 +153,8 @@ def dense_layer(bt: Batch, L: Layer, timer=None):
 
 def variant_layer(bt: Batch, v: Variant, i: int, timer=None):
     L, bf = bt.layers[i], v.bufs[i]
-    B.decode_step(v.p, bt.s, L.q, L.kv.k, L.kv.v, B.kv_layout(L.kv.k), bt.pos, bf.state, bf.plan,
+    kv = L.kv if v.kvs is None else v.kvs[i]
+    B.decode_step(v.p, bt.s, L.q, kv.k, kv.v, kv_layout_of(kv), bt.pos, bf.state, bf.plan,
                   bt.scale, bf.out, bf.logits, bf.workspace, events=timer)
 
 

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.SIGNATURES), "binding and header disagree"
-    assert B.abi_version() == 2
+    assert B.abi_version() == 3
 
 
 def test_status_strings():
@@ -133,3 +133,39 @@ def test_layouts_and_split_config(mode, sinks, shape, par):
     want_ws = pairs * li.max_splits * g * (s.head_dim + 2) * 4 if li.max_splits > 1 else 0
     assert li.workspace_bytes == want_ws == B.workspace_bytes(p, s)
     assert B.window_logits_count(p, s) == s.batch * s.num_q_heads * pl.cap
+
+
+STRUCTS = {
+    "dsa_params": "Params", "dsa_shape": "Shape", "dsa_kv_layout": "KVLayout",
+    "dsa_plan_layout": "PlanLayout", "dsa_state_layout": "StateLayout",
+    "dsa_launch_info": "LaunchInfo",
+}
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structures have the C compiler's size and field
+    offsets for every structure the header declares."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no host C compiler")
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "dsa.h"', "int main(void) {"]
+    for cname, pyname in STRUCTS.items():
+        st = getattr(B, pyname)
+        lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in st._fields_:
+            lines.append(f'  printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run([gcc, "-D__HIP_PLATFORM_AMD__", "-I", inc, "-I", "/opt/rocm/include",
+                    str(src), "-o", str(exe)], check=True)
+    got = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in filter(None, got):
+        cname, field, value = line.split()
+        st = getattr(B, STRUCTS[cname])
+        want = ctypes.sizeof(st) if field == "size" else getattr(st, field).offset
+        assert int(value) == want, (cname, field, value, want)
