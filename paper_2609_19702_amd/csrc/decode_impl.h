@@ -72,6 +72,7 @@ struct KvBf16 {
   static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r) {
     return __builtin_bit_cast(bf16x8, r);
   }
+  static __device__ __forceinline__ uint4 bf16_pairs(const Raw& r) { return r; }
 };
 
 struct KvFp8 {
@@ -103,7 +104,25 @@ struct KvFp8 {
       w[i] = (__float_as_uint(f[2 * i]) >> 16) | (__float_as_uint(f[2 * i + 1]) & 0xffff0000u);
     return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
   }
+  static __device__ __forceinline__ uint4 bf16_pairs(const Raw& r) {
+    return __builtin_bit_cast(uint4, to_bf16(r));
+  }
 };
+
+// q . k over a lane's 8 elements with v_dot2_f32_bf16: bf16 pairs in, fp32
+// accumulation (each bf16 product is exact in fp32).  Both operands are bf16
+// values (an fp8 key is first turned into bf16, exactly).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float dot8_bf16(const uint4& q, const uint4& k) {
+  const uint32_t qa[4] = {q.x, q.y, q.z, q.w};
+  const uint32_t ka[4] = {k.x, k.y, k.z, k.w};
+  float x = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    x = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, qa[i]),
+                                        __builtin_bit_cast(bf16x2_t, ka[i]), x, false);
+  return x;
+}
 
 constexpr int kPre = 8;  // stored skip offsets per lane loaded up front
 
@@ -453,10 +472,29 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && j0 == P);
   }
 
+  // Fused step: a wave whose first tile holds prompt rows issues that tile's
+  // K loads before the ranking below, so they are in flight while the window
+  // rows are ranked (V too would not fit in 128 registers).
+  constexpr bool kHoist = FUSED && !MF;
+  typename KV::Raw kr[U], vr[U];  // the vector-ALU tile's K/V
+  const bool pre = kHoist && wave < P;
+  if constexpr (kHoist) {
+    if (pre) {
+      const int rs = r0 + wave * T;
+      const int re = min(rs + T, pe);
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = rs + u * RPI + rg;
+        const int cr = r < re ? r : 0;  // rows past the tile end read row 0, weight 0
+        kr[u] = KV::load(kb + cr * a.sr);
+      }
+    }
+  }
+
   if constexpr (FUSED) {
-    // Rank every kept window row this wave owns before any wave of the
-    // workgroup loads K/V: the whole workgroup then streams its rows
-    // together instead of the window rows queueing behind the prompt rows.
+    // Rank every kept window row this wave owns before any window tile
+    // loads K/V: the whole workgroup then streams its rows together instead
+    // of the window rows queueing behind the prompt rows.
     for (int j = wave; j < P + Wn; j += nwaves) {
       if (j < P) continue;
       const int rs = wst + (j - P) * T;
@@ -482,11 +520,9 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     if (Wn > 0) __syncthreads();
   }
 
-  float qf[MF ? 1 : G][8];
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    if constexpr (!MF) unpack8(qr[g], qf[g]);
     m[g] = kNegBig;
     l[g] = 0.f;
 #pragma unroll
@@ -514,29 +550,22 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
                                  m_c, l_c, acc, &wl_s[0][0], &p_s[wave][0][0], &alpha_s[wave][0]);
       continue;
     }
-    typename KV::Raw kr[U], vr[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = rs + u * RPI + rg;
       const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
       int cr = 0;  // rows past the tile end read row 0 and get weight 0
       if (r < re) cr = has_win ? a.Lp + wpos : r;
-      kr[u] = KV::load(kb + cr * a.sr);
+      if (!(kHoist && pre && j == wave)) kr[u] = KV::load(kb + cr * a.sr);  // else loaded early
       vr[u] = KV::load(vb + cr * a.sr);
     }
 
     float sc[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      float kf[8];
-      KV::widen(kr[u], kf);
+      const uint4 kw = KV::bf16_pairs(kr[u]);
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float x = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x = fmaf(qf[g][e], kf[e], x);
-        sc[u][g] = group_sum<LPR>(x);
-      }
+      for (int g = 0; g < G; ++g) sc[u][g] = group_sum<LPR>(dot8_bf16(qr[g], kw));
     }
     if (has_win && c == 0) {
 #pragma unroll
@@ -698,8 +727,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
 }
 
+// One query head per KV head: four waves per SIMD stay resident (at most
+// 128 registers), so a small sparse layer runs as a single round of
+// workgroups.  (Larger groups keep their accumulators in registers instead.)
 template <class KV, int D, int G, int U, bool FUSED>
-__global__ __launch_bounds__(kBlock) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G == 1 ? 4 : 1, 8)))
+void decode_kernel(DecodeArgs a) {
   decode_body<KV, D, G, U, FUSED, false>(a);
 }
 
