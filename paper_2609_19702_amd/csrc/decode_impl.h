@@ -72,7 +72,6 @@ struct KvBf16 {
   static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r) {
     return __builtin_bit_cast(bf16x8, r);
   }
-  static __device__ __forceinline__ uint4 bf16_pairs(const Raw& r) { return r; }
 };
 
 struct KvFp8 {
@@ -104,25 +103,7 @@ struct KvFp8 {
       w[i] = (__float_as_uint(f[2 * i]) >> 16) | (__float_as_uint(f[2 * i + 1]) & 0xffff0000u);
     return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
   }
-  static __device__ __forceinline__ uint4 bf16_pairs(const Raw& r) {
-    return __builtin_bit_cast(uint4, to_bf16(r));
-  }
 };
-
-// q . k over a lane's 8 elements with v_dot2_f32_bf16: bf16 pairs in, fp32
-// accumulation (each bf16 product is exact in fp32).  Both operands are bf16
-// values (an fp8 key is first turned into bf16, exactly).
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ float dot8_bf16(const uint4& q, const uint4& k) {
-  const uint32_t qa[4] = {q.x, q.y, q.z, q.w};
-  const uint32_t ka[4] = {k.x, k.y, k.z, k.w};
-  float x = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    x = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, qa[i]),
-                                        __builtin_bit_cast(bf16x2_t, ka[i]), x, false);
-  return x;
-}
 
 constexpr int kPre = 8;  // stored skip offsets per lane loaded up front
 
@@ -265,22 +246,47 @@ __device__ int count_kept(const SkipSet& ss, int lane) {
   return n;
 }
 
-// One 32-row tile of the grouped-head path.  q.K^T runs on
-// v_mfma_f32_16x16x32_bf16: K rows are loaded straight into the A layout
-// (lane l: row l%16, 8 elements per k-step), the group's queries are the B
-// operand, and the C layout leaves head l%16's scores of rows 4*(l/16)+j in
-// lane l.  The softmax statistics stay in that layout; the weights reach the
-// V-layout lanes through a small LDS slice of the wave, and P.V runs in fp32
-// on the vector ALUs (bf16 weights would cost ~2^-9 relative error).
+// Round to the nearest bf16 (ties to even); finite inputs.
+__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Rows of a wave's V tile in LDS are D + kVPad bf16 apart: 32 bytes past a
+// multiple of 128, so the four rows one transposed read touches fall in
+// distinct banks.
+constexpr int kVPad = 16;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// One 32-row tile of the grouped-head path, both products on the matrix
+// cores (v_mfma_f32_16x16x32_bf16).
+//
+// q.K^T: K rows are loaded straight into the A layout (lane l: row l%16,
+// 8 elements per k-step), the group's queries are the B operand, and the C
+// layout leaves head l%16's scores of rows 16*h + 4*(l/16) + j in lane l
+// (h = 0, 1: the tile's two 16-row blocks).
+//
+// P.V: the weights stay where the softmax left them.  Lane l's eight
+// weights (head l%16, rows 4*(l/16) + j and 16 + 4*(l/16) + j) are exactly
+// its A operand once the 32 rows are taken in the order
+// k = 8*q + e -> row 4*q + e (e < 4), 16 + 4*q + e - 4 (e >= 4).  V goes
+// through a per-wave LDS tile and comes back with ds_read_b64_tr_b16 in
+// that same row order as the B operand of each 16-column block; the output
+// accumulates in the C layout (lane l: heads 4*(l/16) + r, column l%16 of
+// the block).  Each weight is split into two bf16 terms (hi + lo, relative
+// error about 2^-17) so the product keeps fp32-level accuracy.
 template <class KV, int D, int G, bool FUSED>
 __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs, int re,
                                           bool has_win, int pos_l, const uint8_t* kmf,
                                           const uint8_t* vb, const bf16x8* qb, int b, int kvh,
                                           int w0, float sl, float sl2, float& m_c, float& l_c,
-                                          float (&acc)[G][8], float* wls, float* ps, float* als) {
+                                          f32x4 (&oacc)[D / 16], float* wls, uint16_t* vt) {
   constexpr int LPR = D / 8, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
   constexpr int NH = T / 16;  // 16-row MFMA blocks per tile
-  const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR;
+  constexpr int VROW = D + kVPad;
+  static_assert(NH == 2, "the P.V row order assumes two 16-row blocks");
+  const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR, c = lane % LPR;
   typename KV::Raw kr[NH][NK];
 #pragma unroll
   for (int h = 0; h < NH; ++h) {
@@ -324,6 +330,10 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
         }
       }
   }
+  // V rows of the tile into the wave's LDS tile, as bf16 (exact for fp8).
+#pragma unroll
+  for (int u = 0; u < UV; ++u)
+    *reinterpret_cast<bf16x8*>(vt + (u * RPI + rg) * VROW + c * 8) = KV::to_bf16(vr[u]);
   // Scores in log2 units, rounded once, so the largest one gets weight
   // exactly 1.
   float s2[NH][4];
@@ -341,37 +351,55 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
   const float alpha = fast_exp2(m_c - mnew);
   m_c = mnew;
   l_c *= alpha;
+  uint32_t ahi[4], alo[4];  // A operands: bf16 pairs of the weights (hi, lo)
 #pragma unroll
   for (int h = 0; h < NH; ++h)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int rl = 16 * h + 4 * lq + j;
-      const float p = rs + rl < re ? fast_exp2(s2[h][j] - mnew) : 0.f;
-      l_c += p;
-      if (lr < G) ps[rl * G + lr] = p;
+    for (int j = 0; j < 4; j += 2) {
+      float p2[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        p2[t] = rs + 16 * h + 4 * lq + j + t < re ? fast_exp2(s2[h][j + t] - mnew) : 0.f;
+        l_c += p2[t];
+      }
+      const uint32_t h0 = bf16_rne_bits(p2[0]), h1 = bf16_rne_bits(p2[1]);
+      const uint32_t l0 = bf16_rne_bits(p2[0] - __uint_as_float(h0 << 16));
+      const uint32_t l1 = bf16_rne_bits(p2[1] - __uint_as_float(h1 << 16));
+      ahi[2 * h + j / 2] = h0 | (h1 << 16);
+      alo[2 * h + j / 2] = l0 | (l1 << 16);
     }
-  if (lr < G && lq == 0) als[lr] = alpha;
-  fence_wave();
-  float al[G];
+  const bf16x8 a_hi = __builtin_bit_cast(bf16x8, make_uint4(ahi[0], ahi[1], ahi[2], ahi[3]));
+  const bf16x8 a_lo = __builtin_bit_cast(bf16x8, make_uint4(alo[0], alo[1], alo[2], alo[3]));
+  // The running output rows are heads 4*(l/16) + r; their rescale factors
+  // live in lanes 4*(l/16) + r.
+  float al[4];
 #pragma unroll
-  for (int g = 0; g < G; ++g) al[g] = als[g];
+  for (int r = 0; r < 4; ++r) al[r] = __shfl(alpha, 4 * lq + r, 64);
 #pragma unroll
-  for (int g = 0; g < G; ++g)
+  for (int cb = 0; cb < D / 16; ++cb)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] *= al[g];
+    for (int r = 0; r < 4; ++r) oacc[cb][r] *= al[r];
+  fence_wave();  // the V tile is written
+  // Transposed reads: lane s of a 16-lane group points at row
+  // 16*hh + 4*(l/16) + s/4, columns 16*cb + 4*(s%4) .. +3; lane n of the
+  // group then holds rows 16*hh + 4*(l/16) + 0..3 of column 16*cb + n.
+  const int s16 = lane & 15;
+  const uint16_t* vsrc = vt + (4 * lq + (s16 >> 2)) * VROW + 4 * (s16 & 3);
 #pragma unroll
-  for (int u = 0; u < UV; ++u) {
-    float vf[8];
-    KV::widen(vr[u], vf);
-    const int rl = u * RPI + rg;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = ps[rl * G + g];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
-    }
+  for (int cb = 0; cb < D / 16; ++cb) {
+    const s16x4 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(vsrc + 16 * cb));
+    const s16x4 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(vsrc + 16 * VROW + 16 * cb));
+    const bf16x8 bv = __builtin_bit_cast(
+        bf16x8, make_uint4(__builtin_bit_cast(uint32_t, __builtin_shufflevector(b0, b0, 0, 1)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(b0, b0, 2, 3)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(b1, b1, 0, 1)),
+                           __builtin_bit_cast(uint32_t, __builtin_shufflevector(b1, b1, 2, 3))));
+    oacc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_hi, bv, oacc[cb], 0, 0, 0);
+    oacc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_lo, bv, oacc[cb], 0, 0, 0);
   }
-  fence_wave();  // the next tile rewrites ps / als
+  fence_wave();  // the next tile rewrites the V tile
 }
 
 template <class KV, int D, int G, int U, bool FUSED, bool MF>
@@ -384,12 +412,18 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   static_assert(T <= 64, "one kept position per lane");
   static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
   constexpr int KS = FUSED ? kMaxFusedSplit : 1;
-  constexpr int PS = MF ? kWaves : 1;
-  __shared__ float red[kWaves][G][D + 2];
+  // The per-wave partial results (red) and, in the MFMA tile, the per-wave
+  // V tiles share one LDS block: the V tiles are dead once every wave has
+  // left the tile loop.
+  constexpr int kRedBytes = kWaves * G * (D + 2) * 4;
+  constexpr int kVtBytes = MF ? kWaves * kMfmaTile * (D + kVPad) * 2 : 0;
+  __shared__ __attribute__((aligned(16)))
+  unsigned char smem[kRedBytes > kVtBytes ? kRedBytes : kVtBytes];
+  float (*red)[G][D + 2] = reinterpret_cast<float (*)[G][D + 2]>(smem);
   __shared__ float wl_s[G][KS];    // fused: window logits of the split
   __shared__ int kp_s[KS];         // fused: kept positions of the split
-  __shared__ float p_s[PS][MF ? kMfmaTile : 1][G];  // MF: softmax weights, C -> V layout
-  __shared__ float alpha_s[PS][G];                  // MF: rescale factors of the tile
+  // MF: one V tile per wave (bf16, rows padded), read back transposed
+  uint16_t* vt_w = reinterpret_cast<uint16_t*>(smem) + (threadIdx.x >> 6) * kMfmaTile * (D + kVPad);
   extern __shared__ uint32_t bm_all[];  // fused: one skip bitmap per wave
 
   const int lane = threadIdx.x & 63;
@@ -520,15 +554,20 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     if (Wn > 0) __syncthreads();
   }
 
+  float qf[MF ? 1 : G][8];
   float m[G], l[G], acc[G][8];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
+    if constexpr (!MF) unpack8(qr[g], qf[g]);
     m[g] = kNegBig;
     l[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
   }
   float m_c = kNegBig, l_c = 0.f;  // MF: running max / partial sum of head lr
+  f32x4 oacc[MF ? D / 16 : 1];     // MF: output, C layout (heads x 16 columns per block)
+#pragma unroll
+  for (int cb = 0; cb < (MF ? D / 16 : 1); ++cb) oacc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int j = wave; j < P + Wn; j += nwaves) {
     const bool dec = j >= P;
@@ -546,8 +585,9 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       if (a.ring && pos_l >= a.Ns) pos_l = a.Ns + (pos_l - a.Ns) % a.ring;  // ring slot
     }
     if constexpr (MF) {
-      mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl, sl2,
-                                 m_c, l_c, acc, &wl_s[0][0], &p_s[wave][0][0], &alpha_s[wave][0]);
+      if constexpr (MF)
+        mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
+                                   sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
       continue;
     }
 #pragma unroll
@@ -563,9 +603,15 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     float sc[U][G];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint4 kw = KV::bf16_pairs(kr[u]);
+      float kf[8];
+      KV::widen(kr[u], kf);
 #pragma unroll
-      for (int g = 0; g < G; ++g) sc[u][g] = group_sum<LPR>(dot8_bf16(qr[g], kw));
+      for (int g = 0; g < G; ++g) {
+        float x = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x = fmaf(qf[g][e], kf[e], x);
+        sc[u][g] = group_sum<LPR>(x);
+      }
     }
     if (has_win && c == 0) {
 #pragma unroll
@@ -623,19 +669,21 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
 
   if constexpr (MF) {
+    __syncthreads();  // every wave is done with its V tile (red aliases it)
     // Head g's running max sits in the lanes with lr == g; its sum is split
-    // over the four lanes lr + 16*q.  The V-layout accumulators of all row
-    // groups share that max, so they merge by plain addition.
+    // over the four lanes lr + 16*q.  The output is already the wave's full
+    // sum in the C layout: lane l holds heads 4*(l/16) + r, column l%16 of
+    // each 16-column block.
     float lt = l_c + shfl_xor(l_c, 16);
     lt += shfl_xor(lt, 32);
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      m[g] = __shfl(m_c, g, 64);
-      l[g] = __shfl(lt, g, 64);
+    for (int cb = 0; cb < D / 16; ++cb)
 #pragma unroll
-      for (int off = LPR; off < 64; off <<= 1)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[g][e] += shfl_xor(acc[g][e], off);
+      for (int r = 0; r < 4; ++r)
+        if (4 * lq + r < G) red[wave][4 * lq + r][16 * cb + lr] = oacc[cb][r];
+    if (lane < G) {
+      red[wave][lane][D] = m_c;
+      red[wave][lane][D + 1] = lt;
     }
   }
   // Merge the row groups of the wave (lanes c, c + LPR, c + 2*LPR, ...).
@@ -657,7 +705,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       m[g] = mn;
     }
   }
-  if (rg == 0) {
+  if (!MF && rg == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
 #pragma unroll
@@ -736,11 +784,11 @@ void decode_kernel(DecodeArgs a) {
   decode_body<KV, D, G, U, FUSED, false>(a);
 }
 
-// The grouped-head (MFMA) tile holds K and V of 32 rows plus G accumulator
-// sets; the occupancy floor keeps three waves per SIMD resident (two for
-// groups of eight, whose accumulators alone take 64 registers).
+// The grouped-head (MFMA) tile holds K and V of 32 rows and the output
+// blocks in registers; the occupancy floor keeps three waves per SIMD
+// resident.
 template <class KV, int D, int G, bool FUSED>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G >= 8 ? 2 : 3, 8)))
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3, 8)))
 void decode_mfma_kernel(DecodeArgs a) {
   decode_body<KV, D, G, 2, FUSED, true>(a);
 }
