@@ -1,7 +1,9 @@
 """Full-size parity: one layer of each workload at its real shape, run
 exactly as the benchmark runs it (same batch, split configuration and
 selection histories built by the library's own phase-2 steps), checked on
-sampled (request, KV head) pairs that the oracle computes one by one.
+sampled (request, KV head) pairs that the oracle computes one by one.  The
+workloads are the three model-shaped ones and cells of the Janus-shaped
+sweep (grid, batch and window at their extremes).
 
 For every sampled pair the oracle replays Algorithm 1 from t = 0 with the
 same per-step queries.  Each phase-2 choice of the GPU must equal the
@@ -31,16 +33,21 @@ def sample_pairs(bt, n):
     phase2 = [b for b in order if N_att - 1 <= pos[b] <= N_r - 2]
     picks = [order[0], order[-1], order[len(order) // 2]] + phase2[:2]
     rng = np.random.default_rng(7)
-    picks += [int(b) for b in rng.choice(len(pos), size=n, replace=False)]
+    picks += [int(b) for b in rng.choice(len(pos), size=min(n, len(pos)), replace=False)]
     out = []
     for i, b in enumerate(dict.fromkeys(picks)):
         out.append((b, int(rng.integers(bt.s.num_kv_heads)) if i % 2 else bt.s.num_kv_heads - 1))
     return out[:n]
 
 
-@pytest.mark.parametrize("name", ["llamagen_xl", "janus_pro_7b", "emu3_8b_gqa"])
+SWEEP = {w.name: w for w in synth.sweep_workloads()}
+SWEEP_CELLS = ["sweep_g24_b1_w64", "sweep_g24_b256_w1024", "sweep_g48_b64_w256",
+               "sweep_g96_b16_w64", "sweep_g48_b1_w1024", "sweep_g96_b256_w1024"]
+
+
+@pytest.mark.parametrize("name", ["llamagen_xl", "janus_pro_7b", "emu3_8b_gqa"] + SWEEP_CELLS)
 def test_fullsize_sampled_parity(name):
-    w = synth.WORKLOADS[name]
+    w = synth.WORKLOADS[name] if name in synth.WORKLOADS else SWEEP[name]
     say("fullsize", name)
     bt = workload.make_batch(w, layers=1)
     workload.build_histories(bt)
