@@ -114,10 +114,11 @@ struct RowRange {
   int flags;  // DSA_FLAG_INACTIVE / DSA_FLAG_POS_CLAMPED
 };
 
+// From the raw decode position t and, for a plan-driven call, the plan's
+// kept count.
 template <bool FUSED>
-__device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pair) {
+__device__ __forceinline__ RowRange row_range_of(const DecodeArgs& a, int t, int plan_count) {
   RowRange r{0, -1, 0};
-  int t = a.pos[b];
   if (t < 0) {
     r.flags = DSA_FLAG_INACTIVE;
     return r;
@@ -132,10 +133,16 @@ __device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pa
   else if (FUSED)
     nwin = min(t + 1, a.Natt);  // the kept count of Algorithm 1 at step t
   else
-    nwin = min(max(a.count[pair], 0), a.plan_cap);
+    nwin = min(max(plan_count, 0), a.plan_cap);
   r.n = a.Lp + nwin;
   r.t = t;
   return r;
+}
+
+template <bool FUSED>
+__device__ __forceinline__ RowRange row_range(const DecodeArgs& a, int b, int pair) {
+  return row_range_of<FUSED>(a, a.pos[b],
+                             (FUSED || a.mode == DSA_MODE_DENSE) ? 0 : a.count[pair]);
 }
 
 // Wave-private skip set of one (request, KV head) for the fused step: the
@@ -161,13 +168,20 @@ struct StateRegs {
   int dv[kPre];
 };
 
-__device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, StateRegs& sr) {
-  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
-  sr.cnt = a.state_cap > 0 ? a.st_count[pair] : 0;
+// The stored offsets only (the count comes with the workgroup's other
+// per-(request, KV head) values).  Branch-free, so the loads stay in flight
+// until the ranking uses them: entries past the capacity re-read entry 0,
+// and a wave that does not need the state (use = false) reads a dummy
+// address (the queries); in both cases the values are never used.
+__device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, bool use,
+                                           StateRegs& sr) {
+  const int cap = use ? a.state_cap : 0;
+  const uint16_t* off = cap > 0 ? a.st_off + static_cast<size_t>(pair) * cap
+                                : reinterpret_cast<const uint16_t*>(a.q);
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
     const int e = lane + 64 * i;
-    sr.dv[i] = e < a.state_cap ? off[e] : 0;
+    sr.dv[i] = off[e < cap ? e : 0];
   }
 }
 
@@ -244,6 +258,30 @@ __device__ int count_kept(const SkipSet& ss, int lane) {
   int n = ss.sk;
   for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64) n += __popcll(__ballot(is_kept(ss, p0 + lane)));
   return n;
+}
+
+// One butterfly step of the log-sum-exp merge of per-lane partial results
+// (running max m, sum l, weighted values acc) across lanes l and l ^ OFF.
+// Every lane whose bit OFF is clear combines (own, partner) in that order.
+template <int OFF, int G>
+__device__ __forceinline__ void merge_groups(float (&m)[G], float (&l)[G], float (&acc)[G][8]) {
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    float m1, m2, l1, l2;
+    xor_pair<OFF>(m[g], m1, m2);
+    xor_pair<OFF>(l[g], l1, l2);
+    const float mn = fmaxf(m1, m2);
+    const float a1 = fast_exp2(m1 - mn);
+    const float a2 = fast_exp2(m2 - mn);
+    l[g] = fmaf(l1, a1, l2 * a2);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float x1, x2;
+      xor_pair<OFF>(acc[g][e], x1, x2);
+      acc[g][e] = fmaf(x1, a1, x2 * a2);
+    }
+    m[g] = mn;
+  }
 }
 
 // Round to the nearest bf16 (ties to even); finite inputs.
@@ -345,8 +383,13 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
       s2[h][j] = rs + 16 * h + 4 * lq + j < re ? sc[h][j] * sl2 : kNegBig;
       mx = fmaxf(mx, s2[h][j]);
     }
-  mx = fmaxf(mx, shfl_xor(mx, 16));
-  mx = fmaxf(mx, shfl_xor(mx, 32));
+  {
+    float x1, x2;
+    xor_pair<16>(mx, x1, x2);
+    mx = fmaxf(x1, x2);
+    xor_pair<32>(mx, x1, x2);
+    mx = fmaxf(x1, x2);
+  }
   const float mnew = fmaxf(m_c, mx);
   const float alpha = fast_exp2(m_c - mnew);
   m_c = mnew;
@@ -436,9 +479,44 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int kvh = pair % a.Hkv;
   const int b = pair / a.Hkv;
 
-  const RowRange rr = row_range<FUSED>(a, b, pair);
-  const int n = rr.n;
+  // The workgroup's small per-(request, KV head) values do not depend on
+  // one another, so they are loaded together, before anything uses them:
+  // the decode position, the plan count or the stored skip count, the row
+  // base and the fp8 scales.  An absent array is replaced by a readable
+  // dummy address (the queries) and its value ignored, which keeps the
+  // loads unconditional.  The stored skip offsets do not depend on the
+  // decode position either: a wave that may own window rows loads them now
+  // too, so the kept set is ready one memory latency sooner.
+  // Queries first: their address depends on nothing loaded.
+  uint4 qr[MF ? 1 : G];
+  if constexpr (!MF) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      qr[g] = *reinterpret_cast<const uint4*>(
+          a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + (lane % LPR) * 8);
+  }
   const int r0 = s * a.C;
+  const int32_t* dummy32 = reinterpret_cast<const int32_t*>(a.q);
+  const bool has_state = FUSED && a.state_cap > 0;
+  const bool has_plan = !FUSED && a.mode != DSA_MODE_DENSE;
+  const int t_raw = a.pos[b];
+  const int cnt_raw = *(has_state ? a.st_count + pair : has_plan ? a.count + pair : dummy32);
+  const int64_t rb_raw =
+      *(a.row_base ? a.row_base + b : reinterpret_cast<const int64_t*>(a.q));
+  const float ks_raw = *(a.ks ? a.ks + pair : reinterpret_cast<const float*>(a.q));
+  const float vs_raw = *(a.vs ? a.vs + pair : reinterpret_cast<const float*>(a.q));
+  StateRegs sreg{};
+  sreg.cnt = has_state ? cnt_raw : 0;
+  if constexpr (FUSED) {
+    const int pe0 = min(r0 + a.C, a.Lp);
+    const int p0 = pe0 > r0 ? (pe0 - r0 + T - 1) / T : 0;  // prompt tiles of an active request
+    const int ws0 = max(r0, a.Lp);
+    const int wmax = r0 + a.C > ws0 ? (r0 + a.C - ws0 + T - 1) / T : 0;  // most window tiles
+    const int j0 = p0 + ((wave - p0) % nwaves + nwaves) % nwaves;
+    load_state(a, pair, lane, has_state && j0 < p0 + wmax, sreg);
+  }
+  const RowRange rr = row_range_of<FUSED>(a, t_raw, cnt_raw);
+  const int n = rr.n;
   if (s > 0 && r0 >= n) return;
   const int r1 = min(n, r0 + a.C);
   const int nsplit = (n + a.C - 1) / a.C;
@@ -447,23 +525,16 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
 
   // Byte offset of this lane's first element (strides arrive in bytes).
   constexpr int E = KV::kBytes;
-  const int64_t base = (a.row_base ? a.row_base[b] * E : static_cast<int64_t>(b) * a.sb) +
+  const int64_t base = (a.row_base ? rb_raw * E : static_cast<int64_t>(b) * a.sb) +
                        static_cast<int64_t>(kvh) * a.sh + c * 8 * E;
   const uint8_t* kb = a.k + base;
   const uint8_t* vb = a.v + base;
   // fp8 caches: the K scale folds into the logit scale, the V scale into
   // the final normalisation (both 1 for bf16).
-  const float sl = a.ks ? a.scale * a.ks[pair] : a.scale;
-  const float sl2 = a.ks ? a.scale_log2 * a.ks[pair] : a.scale_log2;
+  const float sl = a.ks ? a.scale * ks_raw : a.scale;
+  const float sl2 = a.ks ? a.scale_log2 * ks_raw : a.scale_log2;
   const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
 
-  uint4 qr[MF ? 1 : G];
-  if constexpr (!MF) {
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      qr[g] = *reinterpret_cast<const uint4*>(
-          a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + c * 8);
-  }
   // MFMA operands: K in the A layout (lane l: row l%16, elements
   // 8*(l/16) + 32*i .. +7 of k-step i), q^T in the B layout (lane l: query
   // head l%16 of the group, same elements; zero for l%16 >= G).
@@ -493,7 +564,6 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int Wn = r1 > wst ? (r1 - wst + T - 1) / T : 0;
 
   SkipSet ss{};
-  StateRegs sreg{};
   bool have_set = false;
   // The wave holding window rank 0 (the first decode tile of the pair)
   // reports the plan's count and flags, as dsa_plan would.
@@ -502,7 +572,6 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   if constexpr (FUSED) {
     // First window tile of this wave, if it has one.
     const int j0 = P + ((wave - P) % nwaves + nwaves) % nwaves;
-    if (j0 < P + Wn) load_state(a, pair, lane, sreg);
     reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && j0 == P);
   }
 
@@ -524,11 +593,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       }
     }
   }
-
   if constexpr (FUSED) {
-    // Rank every kept window row this wave owns before any window tile
-    // loads K/V: the whole workgroup then streams its rows together instead
-    // of the window rows queueing behind the prompt rows.
+    // Each wave ranks the kept window rows of its own tiles (its own skip
+    // bitmap, its own slice of kp_s), so no wave waits for another: prompt
+    // tiles start loading as soon as the position is known.
     for (int j = wave; j < P + Wn; j += nwaves) {
       if (j < P) continue;
       const int rs = wst + (j - P) * T;
@@ -551,7 +619,6 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
           rep_flags |= DSA_FLAG_COUNT;
       }
     }
-    if (Wn > 0) __syncthreads();
   }
 
   float qf[MF ? 1 : G][8];
@@ -674,8 +741,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     // over the four lanes lr + 16*q.  The output is already the wave's full
     // sum in the C layout: lane l holds heads 4*(l/16) + r, column l%16 of
     // each 16-column block.
-    float lt = l_c + shfl_xor(l_c, 16);
-    lt += shfl_xor(lt, 32);
+    float x1, x2;
+    xor_pair<16>(l_c, x1, x2);
+    float lt = x1 + x2;
+    xor_pair<32>(lt, x1, x2);
+    lt = x1 + x2;
 #pragma unroll
     for (int cb = 0; cb < D / 16; ++cb)
 #pragma unroll
@@ -687,23 +757,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     }
   }
   // Merge the row groups of the wave (lanes c, c + LPR, c + 2*LPR, ...).
-#pragma unroll
-  for (int off = LPR; off < 64 && !MF; off <<= 1) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float m2 = shfl_xor(m[g], off);
-      const float l2 = shfl_xor(l[g], off);
-      const float mn = fmaxf(m[g], m2);
-      const float a1 = fast_exp2(m[g] - mn);
-      const float a2 = fast_exp2(m2 - mn);
-      l[g] = fmaf(l[g], a1, l2 * a2);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x2 = shfl_xor(acc[g][e], off);
-        acc[g][e] = fmaf(acc[g][e], a1, x2 * a2);
-      }
-      m[g] = mn;
-    }
+  if constexpr (!MF) {
+    if constexpr (LPR == 8) merge_groups<8, G>(m, l, acc);
+    merge_groups<16, G>(m, l, acc);
+    merge_groups<32, G>(m, l, acc);
   }
   if (!MF && rg == 0) {
 #pragma unroll
@@ -724,7 +781,9 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr + a.Ns - 2) {
       const int k = rr.t - (a.Natt - 1);
       if (k < a.state_cap) {
-        const int cnt = a.st_count[pair];
+        // The stored count as loaded at the start (only this workgroup
+        // writes it), so the selection waits for no memory.
+        const int cnt = cnt_raw;
         if (cnt < k) {
           if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
         } else {
@@ -759,7 +818,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     const int h = kvh * G + g;
     if (nsplit <= 1) {
       float inv = L > 0.f ? 1.f / L : 0.f;
-      if (a.vs) inv *= a.vs[pair];
+      if (a.vs) inv *= vs_raw;
       float* o = a.out + (static_cast<size_t>(b) * a.Hq + h) * D;
       o[lane] = A0 * inv;
       if constexpr (D == 128) o[lane + 64] = A1 * inv;

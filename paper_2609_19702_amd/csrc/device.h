@@ -45,6 +45,7 @@ constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]: lane ^ 1
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]: lane ^ 2
 constexpr int kDppRowMirror = 0x140;  // lane i <- lane 15 - i
 constexpr int kDppHalfMirror = 0x141; // lane i <- lane 7 - i within each 8-lane half
+constexpr int kDppRowRor8 = 0x128;    // lane i <- lane (i + 8) mod 16: lane ^ 8
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
@@ -66,18 +67,69 @@ __device__ __forceinline__ float group_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// One step of a butterfly across lanes l and l ^ OFF (OFF = 8, 16 or 32)
+// without the LDS crossbar: a DPP row rotate for 8, the gfx950 lane swaps
+// (v_permlane16_swap / v_permlane32_swap) for 16 and 32.  Gives the pair as
+// (first, second) with first the value of the lane whose bit OFF is clear,
+// so every lane of that half sees (own, partner).
+template <int OFF>
+__device__ __forceinline__ void xor_pair(float x, float& first, float& second) {
+  static_assert(OFF == 8 || OFF == 16 || OFF == 32, "butterfly step of 8, 16 or 32 lanes");
+  if constexpr (OFF == 8) {
+    first = x;
+    second = dpp<kDppRowRor8>(x);
+  } else {
+    const uint32_t u = __float_as_uint(x);
+    const auto r = OFF == 16 ? __builtin_amdgcn_permlane16_swap(u, u, false, false)
+                             : __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    first = __uint_as_float(r[0]);
+    second = __uint_as_float(r[1]);
+  }
+}
+
 __device__ __forceinline__ float shfl_xor(float x, int mask) { return __shfl_xor(x, mask, 64); }
 
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+
+// Reductions over the 64 lanes of a wave without the LDS crossbar: two quad
+// permutations, the 8-lane half mirror and the 16-lane mirror (DPP) combine
+// ever larger aligned groups, then the 16- and 32-lane swaps.  The operation
+// must be commutative; every lane ends with the same value.
+template <typename Op>
+__device__ __forceinline__ float wave_allreduce(float x, Op op) {
+  x = op(x, dpp<kDppQuadSwap1>(x));
+  x = op(x, dpp<kDppQuadSwap2>(x));
+  x = op(x, dpp<kDppHalfMirror>(x));
+  x = op(x, dpp<kDppRowMirror>(x));
+  float a, b;
+  xor_pair<16>(x, a, b);
+  x = op(a, b);
+  xor_pair<32>(x, a, b);
+  return op(a, b);
+}
+
+template <typename Op>
+__device__ __forceinline__ int wave_allreduce(int x, Op op) {
+  x = op(x, dpp_i<kDppQuadSwap1>(x));
+  x = op(x, dpp_i<kDppQuadSwap2>(x));
+  x = op(x, dpp_i<kDppHalfMirror>(x));
+  x = op(x, dpp_i<kDppRowMirror>(x));
+  float a, b;
+  xor_pair<16>(__int_as_float(x), a, b);
+  x = op(__float_as_int(a), __float_as_int(b));
+  xor_pair<32>(__int_as_float(x), a, b);
+  return op(__float_as_int(a), __float_as_int(b));
+}
+
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m, 64));
-  return x;
+  return wave_allreduce(x, [](float a, float b) { return fmaxf(a, b); });
 }
 
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m, 64);
-  return x;
+  return wave_allreduce(x, [](float a, float b) { return a + b; });
 }
 
 }  // namespace dsa
@@ -170,13 +222,12 @@ __device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
       argmin_merge(best, jbest, sigma, j);
     }
   }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const float v2 = __shfl_xor(best, m, 64);
-    const int j2 = __shfl_xor(jbest, m, 64);
-    argmin_merge(best, jbest, v2, j2);
-  }
-  return jbest;
+  // The smallest score over the wave, then the smallest index among the
+  // lanes that hold it (each lane's jbest is its smallest index with its
+  // best score, so ties still go to the smallest j).
+  const float m = wave_allreduce(best, [](float a, float b) { return fminf(a, b); });
+  const int jm = best == m ? jbest : 0x7fffffff;
+  return wave_allreduce(jm, [](int a, int b) { return min(a, b); });
 }
 
 }  // namespace dsa
