@@ -503,8 +503,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int cnt_raw = *(has_state ? a.st_count + pair : has_plan ? a.count + pair : dummy32);
   const int64_t rb_raw =
       *(a.row_base ? a.row_base + b : reinterpret_cast<const int64_t*>(a.q));
-  const float ks_raw = *(a.ks ? a.ks + pair : reinterpret_cast<const float*>(a.q));
-  const float vs_raw = *(a.vs ? a.vs + pair : reinterpret_cast<const float*>(a.q));
+  // Scales exist only for fp8 caches (a bf16 call passes none).
+  constexpr bool kScaled = KV::kBytes == 1;
+  const float ks_raw = kScaled ? *(a.ks ? a.ks + pair : reinterpret_cast<const float*>(a.q)) : 1.f;
+  const float vs_raw = kScaled ? *(a.vs ? a.vs + pair : reinterpret_cast<const float*>(a.q)) : 1.f;
   StateRegs sreg{};
   sreg.cnt = has_state ? cnt_raw : 0;
   if constexpr (FUSED) {
@@ -515,6 +517,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     const int j0 = p0 + ((wave - p0) % nwaves + nwaves) % nwaves;
     load_state(a, pair, lane, has_state && j0 < p0 + wmax, sreg);
   }
+  // Settle the scalar values here, all at once: left alone, the compiler
+  // sinks each load to its first use and waits for them one at a time.
+  if constexpr (kScaled)
+    asm volatile("" ::"s"(t_raw), "s"(cnt_raw), "s"(rb_raw), "s"(ks_raw), "s"(vs_raw));
+  else
+    asm volatile("" ::"s"(t_raw), "s"(cnt_raw), "s"(rb_raw));
   const RowRange rr = row_range_of<FUSED>(a, t_raw, cnt_raw);
   const int n = rr.n;
   if (s > 0 && r0 >= n) return;
@@ -531,8 +539,8 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const uint8_t* vb = a.v + base;
   // fp8 caches: the K scale folds into the logit scale, the V scale into
   // the final normalisation (both 1 for bf16).
-  const float sl = a.ks ? a.scale * ks_raw : a.scale;
-  const float sl2 = a.ks ? a.scale_log2 * ks_raw : a.scale_log2;
+  const float sl = kScaled && a.ks ? a.scale * ks_raw : a.scale;
+  const float sl2 = kScaled && a.ks ? a.scale_log2 * ks_raw : a.scale_log2;
   const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
 
   // MFMA operands: K in the A layout (lane l: row l%16, elements
@@ -636,7 +644,9 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
 #pragma unroll
   for (int cb = 0; cb < (MF ? D / 16 : 1); ++cb) oacc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int j = wave; j < P + Wn; j += nwaves) {
+  // One tile of the wave (tile j of the split).  hoisted: its K rows were
+  // loaded before the ranking.
+  auto tile = [&](int j, bool hoisted) {
     const bool dec = j >= P;
     const bool has_win = dec && !dense;
     const int rs = dec ? wst + (j - P) * T : r0 + j * T;
@@ -655,7 +665,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       if constexpr (MF)
         mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
                                    sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
-      continue;
+      return;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -663,9 +673,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
       int cr = 0;  // rows past the tile end read row 0 and get weight 0
       if (r < re) cr = has_win ? a.Lp + wpos : r;
-      if (!(kHoist && pre && j == wave)) kr[u] = KV::load(kb + cr * a.sr);  // else loaded early
+      if (!hoisted) kr[u] = KV::load(kb + cr * a.sr);
       vr[u] = KV::load(vb + cr * a.sr);
     }
+    // Every load of the tile is issued before any arithmetic on it.
+    __builtin_amdgcn_sched_barrier(0);
 
     float sc[U][G];
 #pragma unroll
@@ -726,7 +738,15 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
         for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
       }
     }
+  };
+  // A wave with hoisted K loads runs its first tile outside the loop, so the
+  // loop's registers never overlap loads still in flight.
+  int j = wave;
+  if (kHoist && pre) {
+    tile(j, true);
+    j += nwaves;
   }
+  for (; j < P + Wn; j += nwaves) tile(j, false);
 
   if constexpr (FUSED) {
     if (reporter && lane == 0) {
@@ -818,7 +838,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     const int h = kvh * G + g;
     if (nsplit <= 1) {
       float inv = L > 0.f ? 1.f / L : 0.f;
-      if (a.vs) inv *= vs_raw;
+      if (kScaled && a.vs) inv *= vs_raw;
       float* o = a.out + (static_cast<size_t>(b) * a.Hq + h) * D;
       o[lane] = A0 * inv;
       if constexpr (D == 128) o[lane + 64] = A1 * inv;
