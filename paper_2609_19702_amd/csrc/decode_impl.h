@@ -227,7 +227,11 @@ __device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
 
 // Kept window positions of ranks [lo, hi) (ascending position), written to
 // kp[rank - kp_base] and to the plan.  The cursor only moves forward, so the
-// tiles of a wave (in increasing rank order) share one scan.
+// tiles of a wave (in increasing rank order) share one scan.  The scan reads
+// the bitmap words of kRankBatch chunks of 64 positions at once, so the LDS
+// latency is paid once per batch rather than once per chunk.
+constexpr int kRankBatch = 4;
+
 __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss, int lo, int hi,
                             int* kp, int kp_base) {
   const uint64_t below = (uint64_t(1) << lane) - 1;
@@ -236,19 +240,31 @@ __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss
     kp[r - kp_base] = r;
     plan[r] = r;
   }
-  while (ss.p0 <= ss.t && ss.rank < hi) {
-    const int p = ss.p0 + lane;
-    const bool kept = is_kept(ss, p);
-    const uint64_t mask = __ballot(kept);
-    const int rk = ss.rank + __popcll(mask & below);
-    if (kept && rk >= lo && rk < hi) {
-      kp[rk - kp_base] = p;
-      plan[rk] = p;
+  bool more = ss.p0 <= ss.t && ss.rank < hi;
+  while (more) {
+    bool kept[kRankBatch];
+    uint64_t mask[kRankBatch];
+#pragma unroll
+    for (int i = 0; i < kRankBatch; ++i) kept[i] = is_kept(ss, ss.p0 + 64 * i + lane);
+#pragma unroll
+    for (int i = 0; i < kRankBatch; ++i) mask[i] = __ballot(kept[i]);
+#pragma unroll
+    for (int i = 0; i < kRankBatch && more; ++i) {
+      const int p = ss.p0 + lane;
+      const int rk = ss.rank + __popcll(mask[i] & below);
+      if (kept[i] && rk >= lo && rk < hi) {
+        kp[rk - kp_base] = p;
+        plan[rk] = p;
+      }
+      const int tot = ss.rank + __popcll(mask[i]);
+      if (tot > hi) {  // the chunk reaches past this tile: keep it for the next one
+        more = false;
+      } else {
+        ss.rank = tot;
+        ss.p0 += 64;
+        more = ss.p0 <= ss.t && ss.rank < hi;
+      }
     }
-    const int tot = ss.rank + __popcll(mask);
-    if (tot > hi) break;  // the chunk reaches past this tile: keep it for the next one
-    ss.rank = tot;
-    ss.p0 += 64;
   }
   fence_wave();
 }
@@ -256,7 +272,13 @@ __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss
 // Total kept positions of the window (for the DSA_FLAG_COUNT check).
 __device__ int count_kept(const SkipSet& ss, int lane) {
   int n = ss.sk;
-  for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64) n += __popcll(__ballot(is_kept(ss, p0 + lane)));
+  for (int p0 = ss.t - ss.dmax; p0 <= ss.t; p0 += 64 * kRankBatch) {
+    bool kept[kRankBatch];
+#pragma unroll
+    for (int i = 0; i < kRankBatch; ++i) kept[i] = is_kept(ss, p0 + 64 * i + lane);
+#pragma unroll
+    for (int i = 0; i < kRankBatch; ++i) n += __popcll(__ballot(kept[i]));
+  }
   return n;
 }
 
