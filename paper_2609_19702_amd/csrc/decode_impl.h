@@ -625,8 +625,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
   if constexpr (FUSED) {
     // Each wave ranks the kept window rows of its own tiles (its own skip
-    // bitmap, its own slice of kp_s), so no wave waits for another: prompt
-    // tiles start loading as soon as the position is known.
+    // bitmap, its own slice of kp_s).
     for (int j = wave; j < P + Wn; j += nwaves) {
       if (j < P) continue;
       const int rs = wst + (j - P) * T;
@@ -648,6 +647,13 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
             kept != min(rr.t + 1, a.Natt))
           rep_flags |= DSA_FLAG_COUNT;
       }
+    }
+    // Vector-ALU tile: the prompt waves' V loads (and later tiles) wait until
+    // the window rows are ranked, so the window rows' loads enter each CU's
+    // memory queue ahead of half of the prompt traffic instead of behind all
+    // of it; the hoisted prompt K loads keep the memory busy meanwhile.
+    if constexpr (!MF) {
+      if (Wn > 0 && P > 0) __syncthreads();
     }
   }
 
