@@ -226,8 +226,10 @@ __device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
 }
 
 // Kept window positions of ranks [lo, hi) (ascending position), written to
-// kp[rank - kp_base] and to the plan.  The cursor only moves forward, so the
-// tiles of a wave (in increasing rank order) share one scan.  The scan reads
+// kp[rank - kp_base] (LDS; the plan rows are written from there after the
+// K/V loop, so no store waits behind the loads in the memory queue).  The
+// cursor only moves forward, so the tiles of a wave (in increasing rank
+// order) share one scan.  The scan reads
 // the bitmap words of kRankBatch chunks of 64 positions at once, so the LDS
 // latency is paid once per batch rather than once per chunk.
 constexpr int kRankBatch = 4;
@@ -235,11 +237,8 @@ constexpr int kRankBatch = 4;
 __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss, int lo, int hi,
                             int* kp, int kp_base) {
   const uint64_t below = (uint64_t(1) << lane) - 1;
-  int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
-  for (int r = lo + lane; r < min(hi, ss.sk); r += 64) {  // sink rank r is position r
+  for (int r = lo + lane; r < min(hi, ss.sk); r += 64)  // sink rank r is position r
     kp[r - kp_base] = r;
-    plan[r] = r;
-  }
   bool more = ss.p0 <= ss.t && ss.rank < hi;
   while (more) {
     bool kept[kRankBatch];
@@ -252,10 +251,7 @@ __device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss
     for (int i = 0; i < kRankBatch && more; ++i) {
       const int p = ss.p0 + lane;
       const int rk = ss.rank + __popcll(mask[i] & below);
-      if (kept[i] && rk >= lo && rk < hi) {
-        kp[rk - kp_base] = p;
-        plan[rk] = p;
-      }
+      if (kept[i] && rk >= lo && rk < hi) kp[rk - kp_base] = p;
       const int tot = ss.rank + __popcll(mask[i]);
       if (tot > hi) {  // the chunk reaches past this tile: keep it for the next one
         more = false;
@@ -777,6 +773,14 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   for (; j < P + Wn; j += nwaves) tile(j, false);
 
   if constexpr (FUSED) {
+    // The plan rows of this wave's window tiles, from the ranks in LDS.
+    int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
+    for (int jw = wave; jw < P + Wn; jw += nwaves) {
+      if (jw < P) continue;
+      const int rs = wst + (jw - P) * T;
+      const int re = min(rs + T, r1);
+      if (lane < re - rs) plan[rs - a.Lp + lane] = kp_s[rs - a.Lp + lane - w0];
+    }
     if (reporter && lane == 0) {
       a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
       a.plan_flags[pair] = rep_flags;
