@@ -54,6 +54,11 @@ def parse():
     ap.add_argument("--only", default=None,
                     choices=["fused", "separate", "dense", "diag_sink4", "streaming", "fp8_kv"],
                     help="time one step variant only (shorter profiler runs)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the Janus-shaped sweep (grid x batch x window, diagonal and dense) "
+                         "per layer and print one JSON line per cell instead of the step line")
+    ap.add_argument("--cells", default=None,
+                    help="with --sweep: comma-separated substrings of the cell names to run")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                     help="run a plain device copy of MB megabytes 10 times and exit (the "
                          "reference for scaling the profiler's FETCH_SIZE/WRITE_SIZE)")
@@ -174,6 +179,86 @@ def kernel_times(bt, steps, mode):
     return [a.elapsed_time(b) for row in timers for (a, b) in row]
 
 
+SWEEP_MIN_BYTES = 1 << 30     # rotating layer buffers per cell: at least 1 GiB of KV ...
+SWEEP_MIN_LAYERS = 4          # ... in at least this many layers,
+SWEEP_MAX_BYTES = 100 << 30   # ... and at most this much (then at least 2 layers)
+
+
+def sweep_layers(w):
+    """Distinct layer buffers for one sweep cell, so that no launch finds its
+    KV in the caches left by the previous one."""
+    rows = w.prompt_len + w.decode_len
+    lb = w.batch * w.num_kv_heads * rows * w.head_dim * 2 * 2
+    n = max(SWEEP_MIN_LAYERS, -(-SWEEP_MIN_BYTES // lb))
+    if n * lb > SWEEP_MAX_BYTES:
+        n = max(2, SWEEP_MAX_BYTES // lb)
+    return n
+
+
+def run_sweep(args):
+    """Per-layer decode time of every Janus-shaped sweep cell in diagonal and
+    dense mode: a graph-replayed step over rotating layer buffers (fused
+    ``dsa_decode_step`` per layer, or dense ``dsa_decode_attention``), and the
+    decode kernel's own duration from events bound to it."""
+    import torch
+    from paper_2609_19702_amd import binding as B
+    from paper_2609_19702_amd import synth, workload
+    cells = synth.sweep_workloads()
+    if args.cells:
+        keys = args.cells.split(",")
+        cells = [c for c in cells if any(k in c.name for k in keys)]
+    groups = {}
+    for c in cells:
+        groups.setdefault((c.grid_h, c.batch), []).append(c)
+    steps, warm = max(args.steps, 3), max(args.warmup, 1)
+    for (g, b), ws in groups.items():
+        base = ws[0].with_(name=f"sweep_g{g}_b{b}")
+        nl = sweep_layers(base)
+        t0 = time.time()
+        bt0 = workload.make_batch(base, layers=nl)
+        dense_ms = None
+        for w in ws:
+            bt = workload.with_window(bt0, w.window)
+            workload.build_history_shared(bt)
+            for mode in ("fused",) + (("dense",) if dense_ms is None else ()):
+                for _ in range(warm):
+                    run_step(bt, mode)
+            torch.cuda.synchronize()
+            row = {"cell": w.name, "grid": f"{g}x{g}", "batch": b, "window": bt.p.window,
+                   "n_att": bt.p.n_att, "no_skip": bt.p.n_att >= bt.p.window,
+                   "layers": nl, "positions": "ragged"}
+            res = {}
+            for mode in ("fused",) + (("dense",) if dense_ms is None else ()):
+                gr = capture(bt, mode)
+                gr.replay()
+                torch.cuda.synchronize()
+                ms = timed_steps(bt, steps, mode, gr)
+                kt = statistics.fmean(kernel_times(bt, steps, mode))
+                res[mode] = (ms / nl, kt)
+                del gr
+            if dense_ms is None:
+                dense_ms = res["dense"]
+            sp_bytes = bt.kv_bytes(dense=False) / nl
+            de_bytes = bt.kv_bytes(dense=True) / nl
+            f_ms, f_kt = res["fused"]
+            d_ms, d_kt = dense_ms
+            row.update({
+                "kv_mb_per_layer": sp_bytes / 1e6, "dense_kv_mb_per_layer": de_bytes / 1e6,
+                "layer_us": f_ms * 1e3, "decode_kernel_us": f_kt * 1e3,
+                "kernel_gbps": sp_bytes / (f_kt * 1e-3) / 1e9,
+                "hbm_frac": sp_bytes / (f_kt * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                "dense_layer_us": d_ms * 1e3, "dense_kernel_us": d_kt * 1e3,
+                "dense_kernel_gbps": de_bytes / (d_kt * 1e-3) / 1e9,
+                "speedup_vs_dense": d_ms / f_ms, "ideal_speedup": de_bytes / sp_bytes,
+                "tokens_per_s_per_layer": b / (f_ms * 1e-3),
+            })
+            print(json.dumps(row), flush=True)
+            del bt
+        print(f"# {base.name}: {nl} layers, {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+        del bt0
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -195,6 +280,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": n, "launches": 10}))
+        return
+    if args.sweep:
+        run_sweep(args)
         return
     w = synth.WORKLOADS[args.workload]
     if args.positions:

@@ -171,3 +171,27 @@ def step(bt: Batch, dense: bool = False, timers=None, fused: bool = False,
         else:
             fn = dense_layer if dense else (fused_layer if fused else sparse_layer)
             fn(bt, L, tm)
+
+
+def with_window(bt: Batch, window: int, device="cuda") -> Batch:
+    """The same KV caches, queries and positions under another recent window
+    N_r (and the N_att the sparsity rule gives with it), with fresh per-layer
+    buffers; the selection states start empty."""
+    w = bt.w.with_(window=window, name=f"{bt.w.name}_w{window}")
+    p = B.params_from_sparsity(w.prompt_len, w.grid_h, w.grid_w, w.window, w.sparsity_permille,
+                               B.MODE_DIAGONAL)
+    pd = B.make_params(p.prompt_len, p.grid_h, p.grid_w, p.window, p.n_att, B.MODE_DENSE)
+    layers = [Layer(L.kv, L.q, B.alloc_buffers(p, bt.s, device)) for L in bt.layers]
+    return Batch(w, p, pd, bt.s, bt.pos, bt.pos_host, layers, bt.dense_bufs, bt.scale)
+
+
+def build_history_shared(bt: Batch, device="cuda"):
+    """Selection histories for a timing run: the library's own phase-2 steps
+    build layer 0's skip lists (as ``build_histories``), and every other layer
+    starts from a copy of them.  Each layer still reads its own KV cache; the
+    kept sets are valid Algorithm 1 histories, shared only to save setup
+    time on runs with many layers."""
+    first = bt.layers[0]
+    build_histories(bt, device, bufs=[first.bufs], kvs=[first.kv])
+    for L in bt.layers[1:]:
+        L.bufs.state.copy_(first.bufs.state)
