@@ -224,9 +224,12 @@ def run_sweep(args):
                 for _ in range(warm):
                     run_step(bt, mode)
             torch.cuda.synchronize()
+            info, dinfo = B.launch_info(bt.p, bt.s), B.launch_info(bt.pd, bt.s)
             row = {"cell": w.name, "grid": f"{g}x{g}", "batch": b, "window": bt.p.window,
                    "n_att": bt.p.n_att, "no_skip": bt.p.n_att >= bt.p.window,
-                   "layers": nl, "positions": "ragged"}
+                   "layers": nl, "positions": "ragged",
+                   "launch_threads": info.workgroups * 64 * info.waves_per_group,
+                   "dense_launch_threads": dinfo.workgroups * 64 * dinfo.waves_per_group}
             res = {}
             for mode in ("fused",) + (("dense",) if dense_ms is None else ()):
                 gr = capture(bt, mode)
