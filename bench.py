@@ -20,7 +20,8 @@ the caches.  Prints one JSON line.
 bytes per launch (4*d bytes per attended key per KV head) divided by its
 mean launch time, from HIP events that the extended launch binds to the
 kernel's own start and end, over ``--steps`` further eager steps.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
-of the same workload (``--no-cpu-baseline`` skips it).
+of the same workload on one core, and (``all_cores``) on every host core as a
+pool of single-threaded processes (``--no-cpu-baseline`` skips both).
 """
 
 from __future__ import annotations
@@ -87,17 +88,14 @@ def traffic_for(workload, src_hash):
     return ent.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(bt, seconds):
-    """The fp64 oracle on a bounded sample: a few requests of layer 0, each
-    decode step repeated until about ``seconds`` of CPU time is spent."""
-    import numpy as np
+def oracle_units(bt):
+    """A bounded sample of the workload for the CPU oracle: six requests of
+    layer 0 spread over the decode positions, with a valid selection state
+    each (fp64 numpy arrays)."""
+    import numpy as np  # noqa: F401
     import torch
     from oracle import step as ostep
     from paper_2609_19702_amd import synth
-    try:
-        from threadpoolctl import threadpool_limits
-    except ImportError:  # pragma: no cover
-        threadpool_limits = None
     w, L = bt.w, bt.layers[0]
     order = sorted(range(w.batch), key=lambda b: bt.pos_host[b])
     pick = [order[i * (len(order) - 1) // 5] for i in range(6)]
@@ -105,12 +103,23 @@ def cpu_baseline(bt, seconds):
     qn = L.q.to(torch.float64).cpu().numpy()
     for b in pick:
         t = bt.pos_host[b]
-        k = L.kv.k[b].to(torch.float64).cpu().numpy()
-        v = L.kv.v[b].to(torch.float64).cpu().numpy()
+        k = L.kv.k[b, :, :w.prompt_len + t + 1].to(torch.float64).cpu().numpy()
+        v = L.kv.v[b, :, :w.prompt_len + t + 1].to(torch.float64).cpu().numpy()
         ints = synth.random_ints(w, 0, w.num_kv_heads * w.window, sub=b).tolist()
         st = ostep.random_states(w.num_kv_heads, bt.p.window, bt.p.n_att, t, ints)
         units.append((t, qn[b], k[:, :w.prompt_len], v[:, :w.prompt_len],
                       k[:, w.prompt_len:], v[:, w.prompt_len:], st))
+    return pick, units
+
+
+def oracle_loop(units, scale, seconds):
+    """Run the oracle's decode step over ``units`` until ``seconds`` of wall
+    time are spent on it, numpy on one thread; returns (steps, seconds)."""
+    from oracle import step as ostep
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
     ctx = threadpool_limits(1) if threadpool_limits else None
     done, spent = 0, 0.0
     try:
@@ -118,18 +127,49 @@ def cpu_baseline(bt, seconds):
             for (t, q, Kp, Vp, K, V, st) in units:
                 st2 = copy.deepcopy(st)
                 t0 = time.perf_counter()
-                ostep.request_step(t, q, Kp, Vp, K, V, bt.scale, "diagonal", st2)
+                ostep.request_step(t, q, Kp, Vp, K, V, scale, "diagonal", st2)
                 spent += time.perf_counter() - t0
                 done += 1
     finally:
         if ctx is not None:
             ctx.__exit__(None, None, None)
+    return done, spent
+
+
+def _oracle_worker(args):
+    units, scale, seconds = args
+    return oracle_loop(units, scale, seconds)
+
+
+def cpu_baseline(bt, seconds):
+    """The fp64 oracle on a bounded sample (``oracle_units``), each decode
+    step repeated until about ``seconds`` of CPU time is spent, on one core;
+    then the same sample on every host core (a process pool of one numpy
+    thread per process, at most 16), which adds ``all_cores``."""
+    import multiprocessing as mp
+    w = bt.w
+    pick, units = oracle_units(bt)
+    done, spent = oracle_loop(units, bt.scale, seconds)
     tok_s = done / spent / len(bt.layers)
-    return {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{len(units)} requests of layer 0 (positions "
-                       f"{[bt.pos_host[b] for b in pick]}), one decode step each (attention "
-                       f"for all {w.num_q_heads} heads + selection), repeated {done} times in "
-                       f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
+    res = {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+           "sample": (f"{len(units)} requests of layer 0 (positions "
+                      f"{[bt.pos_host[b] for b in pick]}), one decode step each (attention "
+                      f"for all {w.num_q_heads} heads + selection), repeated {done} times in "
+                      f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
+    cores = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity")
+                       else (os.cpu_count() or 1)))
+    if cores > 1:
+        per = max(2.0, seconds / 2)
+        t0 = time.perf_counter()
+        with mp.get_context("spawn").Pool(cores) as pool:
+            outs = pool.map(_oracle_worker, [(units, bt.scale, per)] * cores)
+        wall = time.perf_counter() - t0
+        steps = sum(d for d, _ in outs)
+        busy = max(sp for _, sp in outs)
+        res["all_cores"] = {"value": steps / busy / len(bt.layers), "cores": cores,
+                            "steps": steps, "seconds_per_worker": busy,
+                            "wall_s_with_startup": wall}
+    return res
 
 
 VARIANTS = {}  # mode name -> workload.Variant, filled by main()
