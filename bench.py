@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="time the Janus-shaped sweep (grid x batch x window, diagonal and dense) "
                          "per layer and print one JSON line per cell instead of the step line")
+    ap.add_argument("--trajectory", action="store_true",
+                    help="time a whole image: every request decodes positions 0 .. H*W-1 over "
+                         "every layer (fused step, and dense mode), one JSON line")
     ap.add_argument("--cells", default=None,
                     help="with --sweep: comma-separated substrings of the cell names to run")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
@@ -302,6 +305,62 @@ def run_sweep(args):
         torch.cuda.empty_cache()
 
 
+def run_trajectory(args):
+    """One whole image per request: decode positions 0 .. H*W-1 in order, every
+    layer per position, starting from empty selection states, so phase 1, the
+    phase-2 selections and phase 3 all occur as often as they do in
+    generation.  Each position's step (all layers) is captured as one HIP
+    graph reading its positions from a device table; the graphs are replayed
+    back to back and timed with events, for the fused step and for dense
+    mode.  The K/V rows of every position are in the cache from the start
+    (the model would write row t just before step t)."""
+    import torch
+    from paper_2609_19702_amd import binding as B
+    from paper_2609_19702_amd import synth, workload
+    w = synth.WORKLOADS[args.workload].with_(positions="last")
+    t0 = time.time()
+    bt = workload.make_batch(w)
+    L_dec = w.decode_len
+    table = torch.arange(L_dec, dtype=torch.int32, device="cuda").repeat_interleave(w.batch)
+    table = table.view(L_dec, w.batch)
+    res = {"metric": "whole-image decode attention time (all positions, all layers)",
+           "workload": f"{w.name}_like", "layers": len(bt.layers), "batch": w.batch,
+           "positions": L_dec, "window": bt.p.window, "n_att": bt.p.n_att,
+           "launch": "hip_graph per position"}
+    for mode in ("fused", "dense"):
+        for L in bt.layers:
+            B.state_reset(bt.p, bt.s, L.bufs.state)
+        graphs = []
+        for t in range(L_dec):
+            bt.pos = table[t]
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run_step(bt, mode)
+            graphs.append(g)
+        torch.cuda.synchronize()
+        for L in bt.layers:  # capture ran nothing; start the trajectory from empty states
+            B.state_reset(bt.p, bt.s, L.bufs.state)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for g in graphs:
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        res[mode] = {"ms": ms, "us_per_position": ms * 1e3 / L_dec,
+                     "tokens_per_s": w.batch * L_dec / (ms * 1e-3)}
+        if mode == "fused":
+            cnt, flg, _ = B.state_views(bt.p, bt.s, bt.layers[0].bufs.state)
+            res["fused"]["skip_entries_per_head"] = int(cnt.max().item())
+            res["fused"]["skip_capacity"] = B.state_layout(bt.p, bt.s).cap
+            res["fused"]["state_flags"] = int(flg.any().item())
+        del graphs
+        print(f"# {mode}: {ms:.1f} ms ({time.time() - t0:.1f}s)", file=sys.stderr, flush=True)
+    res["speedup_vs_dense"] = res["dense"]["ms"] / res["fused"]["ms"]
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -326,6 +385,9 @@ def main():
         return
     if args.sweep:
         run_sweep(args)
+        return
+    if args.trajectory:
+        run_trajectory(args)
         return
     w = synth.WORKLOADS[args.workload]
     if args.positions:
