@@ -646,8 +646,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     }
     // Vector-ALU tile: the prompt waves' V loads (and later tiles) wait until
     // the window rows are ranked, so the window rows' loads enter each CU's
-    // memory queue ahead of half of the prompt traffic instead of behind all
-    // of it; the hoisted prompt K loads keep the memory busy meanwhile.
+    // memory queue ahead of the prompt V traffic instead of behind all of
+    // it; the hoisted prompt K loads keep the memory busy meanwhile.  (As
+    // compiled, a prompt wave also waits for its hoisted K rows before this
+    // barrier: the loop preheader of the ranking waits for the stored
+    // offsets with a vmcnt that, after the conditional hoisted loads, must
+    // count all of them.  Issuing its V loads earlier measured slower.)
     if constexpr (!MF) {
       if (Wn > 0 && P > 0) __syncthreads();
     }
