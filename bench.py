@@ -19,7 +19,10 @@ the caches.  Prints one JSON line.
 ``roofline`` describes the decode kernel (the dominant one): algorithmic K/V
 bytes per launch (4*d bytes per attended key per KV head) divided by its
 mean launch time, from HIP events that the extended launch binds to the
-kernel's own start and end, over ``--steps`` further eager steps.  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
+kernel's own start and end, over ``--steps`` further eager steps.  Each of
+those steps waits behind a spin kernel until the host has issued all of it,
+so its layers run back to back as in the timed graph replays (``--eager``
+times launches as issued, without the spin).  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
 of the same workload on one core, and (``all_cores``) on every host core as a
 pool of single-threaded processes (``--no-cpu-baseline`` skips both).
 """
@@ -209,17 +212,43 @@ def timed_steps(bt, steps, mode, graph):
     return start.elapsed_time(end) / steps
 
 
-def kernel_times(bt, steps, mode):
+def spin_cycles_per_ms():
+    """Rate of torch's spin kernel (``torch.cuda._sleep``), measured."""
+    import torch
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(1000)
+    s.record()
+    torch.cuda._sleep(1_000_000)
+    e.record()
+    torch.cuda.synchronize()
+    return 1_000_000 / max(s.elapsed_time(e), 1e-3)
+
+
+def kernel_times(bt, steps, mode, prefill=True):
     """Per-launch duration (ms) of the split-K decode kernel over ``steps``
-    eager steps, from events bound to the kernel's own start and end."""
+    eager steps, from events bound to the kernel's own start and end.
+
+    Python issues a layer more slowly than the GPU runs it, so launched one by
+    one every kernel would start on an idle GPU.  With ``prefill`` (the
+    default) each step is queued behind a spin kernel that lasts twice the
+    host's time to issue a step, so the layers then run back to back, as they
+    do in the replays of the step's graph.  (Events captured into the graph
+    itself do not give usable times here.)"""
     import torch
     from paper_2609_19702_amd import binding as B
-    timers = [[B.timing_events() for _ in bt.layers] for _ in range(steps)]
+    timers = [[B.timing_events() for _ in bt.layers] for _ in range(steps + 1)]
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run_step(bt, mode, timers=timers[steps])  # the host's time to issue one step
+    host_ms = (time.perf_counter() - t0) * 1e3
+    torch.cuda.synchronize()
+    spin = int(spin_cycles_per_ms() * (2 * host_ms + 0.5)) if prefill else 0
     for k in range(steps):
+        if spin:
+            torch.cuda._sleep(spin)
         run_step(bt, mode, timers=timers[k])
     torch.cuda.synchronize()
-    return [a.elapsed_time(b) for row in timers for (a, b) in row]
+    return [a.elapsed_time(b) for row in timers[:steps] for (a, b) in row]
 
 
 SWEEP_MIN_BYTES = 1 << 30     # rotating layer buffers per cell: at least 1 GiB of KV ...
@@ -417,7 +446,7 @@ def main():
             g.replay()
     torch.cuda.synchronize()
     ms = {m: timed_steps(bt, args.steps, m, graphs[m]) for m in modes}
-    launch = {m: kernel_times(bt, args.steps, m) for m in modes}
+    launch = {m: kernel_times(bt, args.steps, m, prefill=not args.eager) for m in modes}
     if args.only:
         print(json.dumps({"only": args.only, "ms_per_step": ms[args.only],
                           "decode_launch_us": statistics.fmean(launch[args.only]) * 1e3}))
@@ -494,6 +523,7 @@ def main():
             "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
             "kernel": "decode_kernel (fused step)", "bytes_per_launch": per_launch,
             "launches_timed": len(launch_sparse),
+            "launch_timing": "eager" if args.eager else "eager_back_to_back",
             "launch_us": mean_launch_ms * 1e3, "source_hash": src_hash,
         },
         "cpu_baseline": base,
