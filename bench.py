@@ -242,6 +242,7 @@ def kernel_times(bt, steps, mode, prefill=True):
     run_step(bt, mode, timers=timers[steps])  # the host's time to issue one step
     host_ms = (time.perf_counter() - t0) * 1e3
     torch.cuda.synchronize()
+    prefill = prefill and hasattr(torch.cuda, "_sleep")  # private torch API: time as issued without it
     spin = int(spin_cycles_per_ms() * (2 * host_ms + 0.5)) if prefill else 0
     for k in range(steps):
         if spin:
