@@ -525,6 +525,8 @@ def main():
             "kernel": "decode_kernel (fused step)", "bytes_per_launch": per_launch,
             "launches_timed": len(launch_sparse),
             "launch_timing": "eager" if args.eager else "eager_back_to_back",
+            # every kernel of one layer in the timed replays, launch gaps included
+            "layer_us_in_step": ms_sparse * 1e3 / n_layers,
             "launch_us": mean_launch_ms * 1e3, "source_hash": src_hash,
         },
         "cpu_baseline": base,
