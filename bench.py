@@ -72,9 +72,15 @@ def parse():
     return ap.parse_args()
 
 
+KERNEL_SOURCES = ("api.hip", "decode.hip", "decode_fp8.hip", "decode_impl.h", "device.h", "internal.h")
+
+
 def kernel_source_hash():
+    """Hash of the decode kernels' sources and of the host code that picks
+    their launch configuration (split sizes), which the committed counter
+    runs depend on."""
     h = hashlib.sha256()
-    for name in ("decode.hip", "decode_fp8.hip", "decode_impl.h", "device.h", "internal.h"):
+    for name in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2609_19702_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
