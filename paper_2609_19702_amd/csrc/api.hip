@@ -97,12 +97,12 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   const int64_t rows_max = d->Lp + (sparse ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
   // Measured on MI355X: dense splits of ~24 KB for d = 64 (long ragged rows
-  // balance better), ~48 KB for d = 128 and ~96 KB for the grouped-head tile
-  // (fewer partials to merge).  Sparse-mode splits of ~96 KB for every tile:
-  // against ~48 KB, fewer workgroups rebuild the same window ranking and
-  // fewer partials are merged (7-15% on layers of 16 or more requests at
+  // balance better), ~96 KB for d = 128 and ~256 KB for the grouped-head
+  // tile (fewer partials to merge).  Sparse-mode splits of ~96 KB for every
+  // tile: against ~48 KB, fewer workgroups rebuild the same window ranking
+  // and fewer partials are merged (7-15% on layers of 16 or more requests at
   // d = 128, no change below).  The fused step caps a split at 256 rows.
-  const int dense_kb = d->MF ? 96 : (d->D == 64 ? 24 : 48);
+  const int dense_kb = d->MF ? 256 : (d->D == 64 ? 24 : 96);
   const int diag_kb = 96;
   const int64_t split_bytes =
       (sparse ? env_int("DSA_TUNE_SPLIT_KB", diag_kb) : env_int("DSA_TUNE_SPLIT_KB_DENSE", dense_kb)) *
