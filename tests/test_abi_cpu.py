@@ -169,3 +169,32 @@ def test_struct_layouts_match_the_header(tmp_path):
         st = getattr(B, STRUCTS[cname])
         want = ctypes.sizeof(st) if field == "size" else getattr(st, field).offset
         assert int(value) == want, (cname, field, value, want)
+
+
+# The launch configurations the committed profiles and measurements were
+# taken with: (rows per split, splits, workgroups, waves per workgroup,
+# kernel variant) for the three model-shaped workloads at 95% sparsity, in
+# diagonal and dense mode.  A change to the split rule shows up here first.
+BENCH_CONFIGS = {
+    ("llamagen_xl", 1): (192, 1, 1280, 3, 8),
+    ("llamagen_xl", 0): (128, 6, 7680, 3, 8),
+    ("janus_pro_7b", 1): (160, 2, 8192, 4, 8),
+    ("janus_pro_7b", 0): (192, 5, 20480, 4, 8),
+    ("emu3_8b_gqa", 1): (160, 3, 768, 4, 100),
+    ("emu3_8b_gqa", 0): (512, 9, 2304, 4, 100),
+}
+
+
+@pytest.mark.parametrize("name,mode", sorted(BENCH_CONFIGS))
+def test_benchmark_launch_configs(name, mode, monkeypatch):
+    from paper_2609_19702_amd import synth
+    for var in ("DSA_TUNE_UNROLL", "DSA_TUNE_SPLIT_KB", "DSA_TUNE_SPLIT_KB_DENSE",
+                "DSA_TUNE_MIN_WGS", "DSA_TUNE_VALU_GQA"):
+        monkeypatch.delenv(var, raising=False)
+    w = synth.WORKLOADS[name]
+    p = B.params_from_sparsity(w.prompt_len, w.grid_h, w.grid_w, w.window, w.sparsity_permille,
+                               mode=mode, sinks=0)
+    s = B.make_shape(w.batch, w.num_q_heads, w.num_kv_heads, w.head_dim)
+    li = B.launch_info(p, s)
+    got = (li.rows_per_split, li.max_splits, li.workgroups, li.waves_per_group, li.kernel_variant)
+    assert got == BENCH_CONFIGS[(name, mode)]
