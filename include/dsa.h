@@ -198,7 +198,9 @@ typedef struct dsa_state_layout {
   size_t bytes;
 } dsa_state_layout;
 
-/* How dsa_decode_attention splits the keys (for reports and tests). */
+/* How dsa_decode_attention splits the keys (for reports and tests).  The
+ * split rule is fixed when the library is built: it depends on the
+ * parameters and the shape of a call and on nothing else. */
 typedef struct dsa_launch_info {
   int32_t rows_per_split;  /* C: keys per split workgroup                   */
   int32_t max_splits;      /* S: splits per (request, KV head) at most      */
@@ -317,12 +319,14 @@ DSA_API dsa_status dsa_decode_attention(const dsa_params* p, const dsa_shape* s,
                                         hipStream_t stream);
 
 /*
- * dsa_decode_attention with its split-K kernel launched so that the two
- * events receive that kernel's own start and end timestamps (the AMD
- * extended launch); hipEventElapsedTime(decode_start, decode_stop) is then
- * the kernel's execution time, without queueing or launch gaps.  The events
- * must already exist (hipEventCreate).  For profiling tools; not usable
- * inside a HIP graph capture.  Errors as dsa_decode_attention, and
+ * dsa_decode_attention with its kernels launched so that decode_start
+ * receives the split-K kernel's own start timestamp and decode_stop the end
+ * timestamp of the last kernel of the call (the split-K kernel, or the
+ * combine when a request is split), through the AMD extended launch;
+ * hipEventElapsedTime(decode_start, decode_stop) is then the call's
+ * execution time on the device, without the queueing ahead of it.  The
+ * events must already exist (hipEventCreate).  For profiling tools; not
+ * usable inside a HIP graph capture.  Errors as dsa_decode_attention, and
  * INVALID_ARG for a NULL event.
  */
 DSA_API dsa_status dsa_decode_attention_timed(const dsa_params* p, const dsa_shape* s,
@@ -361,8 +365,9 @@ DSA_API dsa_status dsa_decode_step(const dsa_params* p, const dsa_shape* s, cons
                                    float* d_window_logits, void* d_ws, size_t ws_bytes,
                                    hipStream_t stream);
 
-/* dsa_decode_step with the split kernel's own start/end timestamps recorded
- * into two existing events (as dsa_decode_attention_timed). */
+/* dsa_decode_step with the start of its split-K kernel and the end of its
+ * last kernel recorded into two existing events (as
+ * dsa_decode_attention_timed). */
 DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s, const void* d_q,
                                          const void* d_k, const void* d_v,
                                          const dsa_kv_layout* kv, const int32_t* d_decode_pos,

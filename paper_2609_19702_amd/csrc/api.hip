@@ -1,7 +1,6 @@
 // Host side of the C ABI: argument validation, buffer layouts, the split
 // configuration of the decode kernel, and the extern "C" entry points.
 #include <cmath>
-#include <cstdlib>
 
 #include "internal.h"
 
@@ -9,14 +8,6 @@ namespace dsa {
 namespace {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
-
-int env_int(const char* name, int fallback) {
-  const char* v = std::getenv(name);
-  if (!v || !*v) return fallback;
-  char* end = nullptr;
-  long x = std::strtol(v, &end, 10);
-  return (end && *end == 0 && x > 0 && x < (1 << 20)) ? static_cast<int>(x) : fallback;
-}
 
 }  // namespace
 
@@ -84,15 +75,13 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
 
   // Split configuration of the decode kernel.  A wave issues U loads of
   // 512/d rows each (one tile) before consuming them; a split holds C rows
-  // (a multiple of the tile) and aims at ~48 KB of K+V so every request is
-  // cut into a few workgroups and the grid keeps enough loads in flight.
+  // (a multiple of the tile), so every request is cut into a few workgroups
+  // and the grid keeps enough loads in flight.  Every choice below is a
+  // build-time constant (internal.h), so the launch shape and the workspace
+  // size depend on the parameters and the shape alone.
   const int rows_per_instr = 512 / d->D;  // 8 for d=64, 4 for d=128
-  const int u_default = G >= 8 ? 2 : (G >= 4 ? 4 : 8);
-  const int u_env = env_int("DSA_TUNE_UNROLL", u_default);
-  d->U = (u_env == 2 || u_env == 4 || u_env == 8) ? u_env : u_default;
-  // Grouped query heads take the MFMA tile (q.K^T on matrix cores) unless
-  // DSA_TUNE_VALU_GQA=1 asks for the vector-ALU tile.
-  d->MF = G >= 2 && env_int("DSA_TUNE_VALU_GQA", 0) != 1;
+  d->MF = uses_mfma_tile(G);
+  d->U = unroll_of(G);
   const int block_rows = d->MF ? kMfmaTile : rows_per_instr * d->U;
   const int64_t rows_max = d->Lp + (sparse ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
@@ -101,18 +90,15 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   // tile (fewer partials to merge).  Sparse-mode splits of ~96 KB for every
   // tile: against ~48 KB, fewer workgroups rebuild the same window ranking
   // and fewer partials are merged (7-15% on layers of 16 or more requests at
-  // d = 128, no change below).  The fused step caps a split at 256 rows.
-  const int dense_kb = d->MF ? 256 : (d->D == 64 ? 24 : 96);
-  const int diag_kb = 96;
-  const int64_t split_bytes =
-      (sparse ? env_int("DSA_TUNE_SPLIT_KB", diag_kb) : env_int("DSA_TUNE_SPLIT_KB_DENSE", dense_kb)) *
-      int64_t(1024);
+  // d = 128, no change below).  The fused step caps a split at
+  // kMaxFusedSplit rows.
+  const int dense_kb = d->MF ? kSplitKbDenseMfma : (d->D == 64 ? kSplitKbDense64 : kSplitKbDense128);
+  const int64_t split_bytes = (sparse ? kSplitKbSparse : dense_kb) * int64_t(1024);
   int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
   if (sparse) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
-  const int64_t min_wgs = env_int("DSA_TUNE_MIN_WGS", 512);
-  if (pairs * S < min_wgs) {
-    const int64_t want = (min_wgs + pairs - 1) / pairs;
+  if (pairs * S < kMinWorkgroups) {
+    const int64_t want = (kMinWorkgroups + pairs - 1) / pairs;
     const int64_t most = std::max<int64_t>(1, (rows_max + block_rows - 1) / block_rows);
     S = std::max<int64_t>(S, std::min(want, most));
   }

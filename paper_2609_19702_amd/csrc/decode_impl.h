@@ -1036,26 +1036,29 @@ void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEven
 template <class KV, int D, int G, bool FUSED>
 hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                      hipEvent_t t1) {
-  if constexpr (G >= 2) {
-    if (d.MF) {
-      launch_split<KV, D, G, 2, FUSED, true>(d, a, st, t0, t1);
-      goto launched;
-    }
-  }
-  switch (d.U) {
-    case 8: launch_split<KV, D, G, 8, FUSED, false>(d, a, st, t0, t1); break;
-    case 4: launch_split<KV, D, G, 4, FUSED, false>(d, a, st, t0, t1); break;
-    default: launch_split<KV, D, G, 2, FUSED, false>(d, a, st, t0, t1); break;
-  }
-launched:
+  // With several splits the stop event goes to the combine, so a timed call
+  // covers every kernel it launches.
+  const bool split = d.S > 1;
+  if constexpr (uses_mfma_tile(G))
+    launch_split<KV, D, G, 2, FUSED, true>(d, a, st, t0, split ? nullptr : t1);
+  else
+    launch_split<KV, D, G, unroll_of(G), FUSED, false>(d, a, st, t0, split ? nullptr : t1);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || d.S <= 1) return e;
+  if (e != hipSuccess || !split) return e;
   if (FUSED) {
     constexpr int cw = G < kCombineWaves ? G : kCombineWaves;
-    combine_select_kernel<D, G><<<d.B * d.Hkv, 64 * (cw + 1), 0, st>>>(a);
+    if (t1)
+      hipExtLaunchKernelGGL(combine_select_kernel<D, G>, dim3(d.B * d.Hkv), dim3(64 * (cw + 1)), 0,
+                            st, nullptr, t1, 0, a);
+    else
+      combine_select_kernel<D, G><<<d.B * d.Hkv, 64 * (cw + 1), 0, st>>>(a);
   } else {
     const int cgrid = (d.B * d.Hq + kWaves - 1) / kWaves;
-    combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
+    if (t1)
+      hipExtLaunchKernelGGL(combine_kernel<D>, dim3(cgrid), dim3(kBlock), 0, st, nullptr, t1, 0, a,
+                            G);
+    else
+      combine_kernel<D><<<cgrid, kBlock, 0, st>>>(a, G);
   }
   return hipGetLastError();
 }

@@ -23,20 +23,63 @@ struct Derived {
   dsa_plan_layout plan;
   dsa_state_layout state;
   int rows_max;   // prompt rows + the most decode rows one request can attend
-  int U;          // loads in flight per wave per operand (unroll)
+  int U;          // loads in flight per wave per operand (unroll_of(G))
   int C;          // rows per split workgroup
   int S;          // splits per (request, KV head), upper bound
   int NW;         // waves per decode workgroup (1..kWaves)
-  bool MF;        // grouped query heads: q.K^T on MFMA
+  bool MF;        // grouped query heads on the MFMA tile (uses_mfma_tile(G))
   size_t ws_bytes;
 };
 
 dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 
+// Launch-shape choices, measured on MI355X and fixed at build time: a call's
+// launch configuration and workspace size depend only on its parameters and
+// shape.  A tuning build may override any of them with -D.
+#ifndef DSA_TUNE_SPLIT_KB
+#define DSA_TUNE_SPLIT_KB 96  // K+V bytes per split workgroup, sparse modes
+#endif
+#ifndef DSA_TUNE_SPLIT_KB_DENSE_64
+#define DSA_TUNE_SPLIT_KB_DENSE_64 24  // dense mode, d = 64, one query head per KV head
+#endif
+#ifndef DSA_TUNE_SPLIT_KB_DENSE_128
+#define DSA_TUNE_SPLIT_KB_DENSE_128 96  // dense mode, d = 128, one query head per KV head
+#endif
+#ifndef DSA_TUNE_SPLIT_KB_DENSE_MFMA
+#define DSA_TUNE_SPLIT_KB_DENSE_MFMA 256  // dense mode, grouped query heads
+#endif
+#ifndef DSA_TUNE_MIN_WGS
+#define DSA_TUNE_MIN_WGS 512  // split further while a launch has fewer workgroups
+#endif
+#ifndef DSA_TUNE_MAX_FUSED_SPLIT
+#define DSA_TUNE_MAX_FUSED_SPLIT 256  // rows per sparse-mode split (the fused step keeps them in LDS)
+#endif
+#ifndef DSA_TUNE_UNROLL
+#define DSA_TUNE_UNROLL 0  // loads in flight per wave (2, 4 or 8); 0: by group size
+#endif
+#ifndef DSA_TUNE_VALU_GQA
+#define DSA_TUNE_VALU_GQA 0  // 1: grouped query heads on the vector-ALU tile instead of MFMA
+#endif
+
 constexpr int kWaves = 4;          // waves per workgroup in every kernel
 constexpr int kBlock = 64 * kWaves;
 constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
-constexpr int kMaxFusedSplit = 256;  // rows per diagonal-mode split (fused step keeps them in LDS)
+constexpr int kMaxFusedSplit = DSA_TUNE_MAX_FUSED_SPLIT;
+constexpr int kSplitKbSparse = DSA_TUNE_SPLIT_KB;
+constexpr int kSplitKbDense64 = DSA_TUNE_SPLIT_KB_DENSE_64;
+constexpr int kSplitKbDense128 = DSA_TUNE_SPLIT_KB_DENSE_128;
+constexpr int kSplitKbDenseMfma = DSA_TUNE_SPLIT_KB_DENSE_MFMA;
+constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
+static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
+
+// Grouped query heads take the MFMA tile (q.K^T and P.V on matrix cores).
+constexpr bool uses_mfma_tile(int G) { return G >= 2 && !DSA_TUNE_VALU_GQA; }
+// Loads in flight per wave and operand on the vector-ALU tile.
+constexpr int unroll_of(int G) {
+  return (DSA_TUNE_UNROLL == 2 || DSA_TUNE_UNROLL == 4 || DSA_TUNE_UNROLL == 8)
+             ? DSA_TUNE_UNROLL
+             : (G >= 8 ? 2 : (G >= 4 ? 4 : 8));
+}
 constexpr int kMaxFusedWindow = 16384;  // N_r of the fused step (skip bitmap per wave in LDS)
 constexpr float kNegBig = -1.0e30f;  // "no score yet": finite, so exp2 of a difference is 0
 

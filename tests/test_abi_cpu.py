@@ -186,11 +186,8 @@ BENCH_CONFIGS = {
 
 
 @pytest.mark.parametrize("name,mode", sorted(BENCH_CONFIGS))
-def test_benchmark_launch_configs(name, mode, monkeypatch):
+def test_benchmark_launch_configs(name, mode):
     from paper_2609_19702_amd import synth
-    for var in ("DSA_TUNE_UNROLL", "DSA_TUNE_SPLIT_KB", "DSA_TUNE_SPLIT_KB_DENSE",
-                "DSA_TUNE_MIN_WGS", "DSA_TUNE_VALU_GQA"):
-        monkeypatch.delenv(var, raising=False)
     w = synth.WORKLOADS[name]
     p = B.params_from_sparsity(w.prompt_len, w.grid_h, w.grid_w, w.window, w.sparsity_permille,
                                mode=mode, sinks=0)

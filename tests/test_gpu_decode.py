@@ -123,19 +123,33 @@ def test_constant_values_and_unused_slot():
     assert torch.allclose(out[2], torch.ones_like(out[2]), atol=2e-6)
 
 
-def test_split_size_invariance(monkeypatch):
-    """Different split sizes merge to the same attention (within fp32)."""
-    case = (2, 8, 2, 128, 300, 12, 12, 100, 50, 0.0)
-    outs = []
-    for kb in ("8", "48", "512"):
-        monkeypatch.setenv("DSA_TUNE_SPLIT_KB", kb)
-        w, kv, q, ts, p, s, states = make_case(case, B.MODE_DENSE, seed=9)
-        info = B.launch_info(p, s)
-        say("split KB", kb, "splits", info.max_splits)
-        pos = torch.tensor(ts, dtype=torch.int32, device=DEV)
-        outs.append(run_layer(p, s, q, kv, pos).out.cpu().double())
-    for o in outs[1:]:
+def test_split_size_invariance():
+    """The same request merged from different numbers of splits gives the
+    same attention (within fp32) and matches the oracle.  The split rule
+    depends only on the shape, so the request is placed in batches of 1, 32
+    and 128 copies: the smaller the batch, the more splits per request."""
+    case = (1, 8, 2, 128, 300, 12, 12, 100, 50, 0.0)
+    w, kv, q, ts, p, s, states = make_case(case, B.MODE_DENSE, seed=9)
+    ref, _ = oracle_outputs(w, kv, q, ts, p, s, states, B.MODE_DENSE)
+    outs, splits = [], []
+    for nb in (1, 32, 128):
+        sb = B.make_shape(nb, s.num_q_heads, s.num_kv_heads, s.head_dim)
+        kvb = synth.LayerKV(kv.k.expand(nb, -1, -1, -1).contiguous(),
+                            kv.v.expand(nb, -1, -1, -1).contiguous(), kv.rows)
+        qb = q.expand(nb, -1, -1).contiguous()
+        info = B.launch_info(p, sb)
+        splits.append(info.max_splits)
+        say("batch", nb, "splits", info.max_splits)
+        pos = torch.tensor(ts * nb, dtype=torch.int32, device=DEV)
+        o = run_layer(p, sb, qb, kvb, pos).out.cpu().double()
+        for b in range(nb):
+            assert torch.equal(o[b], o[0])
+        outs.append(o[0])
+    assert len(set(splits)) == 3
+    for o in outs:
         assert (o - outs[0]).abs().max() <= 1e-5 * outs[0].abs().max()
+        for h in range(s.num_q_heads):
+            assert rel_err(o[h].numpy(), ref[0, h]) <= TOL
 
 
 def test_token_major_layout_with_row_base():

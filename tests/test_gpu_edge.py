@@ -4,8 +4,6 @@
   plan beyond it (checked against the oracle on a few pairs and against
   properties that hold at any size: count, order, window, skipped offsets);
 * every slot unused; no prompt with a single key; N_att = 1;
-* the vector-ALU tile for grouped heads (DSA_TUNE_VALU_GQA=1) against the
-  oracle and against the fused step;
 * state reset of a subset of requests;
 * two independent layers on two streams at once;
 * argument errors of the fused step.
@@ -142,40 +140,6 @@ def test_all_slots_unused_and_single_key():
         for b in (0, 1):
             for h in range(2):
                 assert torch.equal(bufs.out[b, h], kv.v[b, h, 0].float())
-
-
-def test_valu_tile_for_grouped_heads(monkeypatch):
-    monkeypatch.setenv("DSA_TUNE_VALU_GQA", "1")
-    w = synth.Workload("valu_gqa", 2, 6, 16, 4, 128, 40, 12, 12, 60, sparsity_permille=900,
-                       outlier_frac=0.01)
-    bt = workload.make_batch(w)
-    assert B.launch_info(bt.p, bt.s).kernel_variant != 100
-    workload.build_histories(bt)
-    state0 = [Lr.bufs.state.clone() for Lr in bt.layers]
-    workload.step(bt)
-    ref = [(Lr.bufs.out.clone(), Lr.bufs.state.clone()) for Lr in bt.layers]
-    for Lr, st in zip(bt.layers, state0):
-        Lr.bufs.state.copy_(st)
-    workload.step(bt, fused=True)
-    torch.cuda.synchronize()
-    for Lr, (o, st) in zip(bt.layers, ref):
-        assert torch.equal(Lr.bufs.out, o) and torch.equal(Lr.bufs.state, st)
-    # outputs of layer 0 against the oracle, over the kept sets the plan reports
-    L0 = bt.layers[0]
-    cnt, _, idx = (x.cpu().numpy() for x in B.plan_views(bt.p, bt.s, L0.bufs.plan))
-    qn = L0.q.double().cpu().numpy()
-    out = L0.bufs.out.double().cpu().numpy()
-    from oracle import attention
-    for b in range(w.batch):
-        if bt.pos_host[b] < 0:
-            continue
-        Kp, Vp, K, V = request_arrays(L0.kv, b, w.prompt_len)
-        for h in range(4):
-            kept = idx[b * 4 + h, :cnt[b * 4 + h]].tolist()
-            keys, vals = np.concatenate([Kp[h], K[h][kept]]), np.concatenate([Vp[h], V[h][kept]])
-            for i in range(4):
-                ref_o, _ = attention.attend(qn[b, h * 4 + i], keys, vals, bt.scale)
-                assert rel_err(out[b, h * 4 + i], ref_o) <= TOL
 
 
 def test_state_reset_mask():
