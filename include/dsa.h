@@ -6,7 +6,7 @@
  * image generator with the kept-KV selection of Algorithm 1 of the paper
  * (section 4, "Diagonal-Aware Sparse Attention"):
  *
- *   - the prompt KV (L_p rows) is always attended in full;
+ *   - every step's keys include all L_p prompt rows;
  *   - inside a recent window of N_r decode positions, a per-head list of
  *     skipped entries grows by one per step during phase 2 (an argmin of the
  *     window softmax) and then stays fixed; because both the list entries and
@@ -139,10 +139,10 @@ typedef struct dsa_shape {
  * L_p .. L_p + S - 1 (S = 0 in dense mode) and position j >= S lives in row
  * L_p + S + ((j - S) mod (R - S)), overwriting position j - (R - S).  In
  * diagonal mode this is the physical form of Algorithm 1's eviction (phase 3
- * drops K[t - N_r]; section 4, "Cost analysis": the footprint is bounded by
- * N_r + L_p) and needs R >= S + N_r; window mode needs R >= N_att; dense
- * mode reads every decode row, so a ring must hold R >= H*W there.  A ring
- * of R >= H*W rows is the linear cache.
+ * drops K[t - N_r], so per section 4, "Cost analysis", no more than
+ * L_p + N_r rows of a head are ever live) and needs R >= S + N_r; window
+ * mode needs R >= N_att; dense mode reads every decode row, so a ring must
+ * hold R >= H*W there.  A ring of R >= H*W rows is the linear cache.
  * A row holds head_dim contiguous elements of type dtype:
  *   DSA_KV_BF16      2 bytes each; d_k_scale and d_v_scale must be NULL.
  *   DSA_KV_FP8_E4M3  1 byte each; element value = E4M3 value of the byte

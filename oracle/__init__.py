@@ -29,6 +29,14 @@ Sparse Attention", Algorithm 1 and the "Detailed explanation" paragraph):
 * ``fp8``       -- exact decoding of an fp8 (OCP E4M3) KV cache with per-
                    (request, KV head) scales, the KV quantization the paper
                    calls orthogonal to its method (section 6).
+* ``coracle``   -- the same Algorithm 1 and decode step restated in plain C
+                   (``oracle/c/dsa_oracle.c``, fp64, OpenMP over KV heads),
+                   for long selection histories and the timed CPU baseline;
+                   pinned to the Python oracle and the worked example.
+* ``tieband``   -- bounds of the fp32 rounding of the phase-2 scores, which
+                   decide when a device's different argmin is still a
+                   correct pick (a near tie); pinned by simulating the fp32
+                   arithmetic it bounds.
 
 Parity status: every function is pinned in ``tests/test_oracle_*.py`` except
 the GQA aggregation of the selection weights (one skip set per KV head, score
@@ -37,4 +45,4 @@ reduction to the paper's per-head rule at group size 1 is pinned, the rest is
 "parity unpinned".
 """
 
-from . import alg1, attention, fp8, params, step  # noqa: F401
+from . import alg1, attention, fp8, params, step, tieband  # noqa: F401

@@ -57,48 +57,58 @@ class HeadState:
         if not (1 <= self.N_att <= self.N_r):
             raise ValueError("Algorithm 1 needs 1 <= N_att <= N_r")
 
+    def phase(self, t: int) -> int:
+        """Which of the algorithm's three regimes step ``t`` is in: 1 before
+        the first selection (``t < N_att - 1``), 2 while the window still
+        grows (``t < N_r``), 3 once the window slides."""
+        if t < self.N_att - 1:
+            return 1
+        return 2 if t < self.N_r else 3
+
+    def needs_choice(self, t: int) -> bool:
+        """True when step ``t`` (about to run) adds a skip entry: only in
+        phase 2, and only until the list holds ``N_r - N_att`` entries."""
+        return self.phase(t) == 2 and len(self.skip_idx) < self.N_r - self.N_att
+
+    def _advance(self, t: int, phase: int) -> None:
+        """State changes at the start of step ``t``: once the window slides,
+        its oldest position ``t - N_r`` leaves the cache; from phase 2 on,
+        every skipped position moves one step along its diagonal (+1)."""
+        if phase == 3:
+            self.evicted.add(t - self.N_r)
+        if phase >= 2:
+            self.skip_idx = [j + 1 for j in self.skip_idx]
+
+    def kept(self, t: int) -> List[int]:
+        """Decode positions step ``t`` attends, ascending: the window
+        ``[max(0, t - N_r), t]`` minus what was evicted and what is skipped."""
+        gone = self.evicted | set(self.skip_idx)
+        return [j for j in range(max(0, t - self.N_r), t + 1) if j not in gone]
+
     def step(self, t: int, choose: Optional[Chooser]) -> StepRecord:
         """Run decode step ``t`` and return what it attends.
 
-        ``choose`` is called only when the algorithm selects a new skip entry
-        (phase 2 with ``|skip_idx| < N_r - N_att``).  It receives ``t`` and
-        the kept list ``idx`` and returns ``j*``, an index into ``idx``.
-        """
-        N_r, N_att = self.N_r, self.N_att
-        window = list(range(max(0, t - N_r), t + 1))
+        ``choose`` is called only when the step adds a skip entry
+        (``needs_choice``).  It receives ``t`` and the kept list ``idx`` and
+        returns ``j*``, an index into ``idx``.  The entry it names joins the
+        skip list after ``idx`` was formed, so it is still attended at step
+        ``t``."""
+        phase = self.phase(t)
+        adds = self.needs_choice(t)
+        self._advance(t, phase)
+        used_skip = list(self.skip_idx)
+        idx = self.kept(t)
         selected = None
-        if t < N_att - 1:
-            # Phase 1: full attention over the window.
-            phase = 1
-            idx = list(window)
-        elif t < N_r:
-            # Phase 2: shift, exclude, attend, then grow the skip set.
-            phase = 2
-            self.skip_idx = [j + 1 for j in self.skip_idx]
-            skip = set(self.skip_idx)
-            idx = [j for j in window if j not in skip]
-            if len(self.skip_idx) < N_r - N_att:
-                if choose is None:
-                    raise ValueError(f"step {t} needs a choice but no chooser was given")
-                j_star = int(choose(t, list(idx)))
-                if not (0 <= j_star < len(idx)):
-                    raise ValueError("chooser returned an index outside idx")
-                selected = idx[j_star]
-                self.skip_idx.append(selected)
-        else:
-            # Phase 3: evict the oldest KV, shift, exclude, attend.
-            phase = 3
-            self.evicted.add(t - N_r)
-            self.skip_idx = [j + 1 for j in self.skip_idx]
-            skip = set(self.skip_idx)
-            idx = [j for j in window if j not in skip and j not in self.evicted]
-        used_skip = list(self.skip_idx) if selected is None else list(self.skip_idx[:-1])
-        return StepRecord(t=t, phase=phase, window=window, skip_idx=used_skip,
-                          idx=idx, selected=selected)
-
-    def needs_choice(self, t: int) -> bool:
-        """True when step ``t`` (about to run) will call the chooser."""
-        return (self.N_att - 1 <= t < self.N_r) and len(self.skip_idx) < self.N_r - self.N_att
+        if adds:
+            if choose is None:
+                raise ValueError(f"step {t} needs a choice but no chooser was given")
+            j_star = int(choose(t, list(idx)))
+            if not (0 <= j_star < len(idx)):
+                raise ValueError("chooser returned an index outside idx")
+            selected = idx[j_star]
+            self.skip_idx.append(selected)
+        return StepRecord(t=t, phase=phase, window=list(range(max(0, t - self.N_r), t + 1)),
+                          skip_idx=used_skip, idx=idx, selected=selected)
 
 
 def run(N_r: int, N_att: int, T: int, choose: Optional[Chooser]) -> List[StepRecord]:

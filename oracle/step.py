@@ -132,27 +132,6 @@ def trajectory(Q, Kp, Vp, K, V, scale: float, N_r: int, N_att: int, mode: str = 
             for t in range(T)]
 
 
-def replay_states(Q_steps, K, scale: float, N_r: int, N_att: int, t_end: int,
-                  num_q_heads: int) -> List[alg1.HeadState]:
-    """Selection states of one request after steps ``0 .. t_end-1``.
-
-    Only phase-2 steps change the skip list beyond the shift, and only their
-    window weights are needed, so this runs Algorithm 1 with the attention
-    argmin but skips the attention output.  ``Q_steps[t]`` is ``[Hq, d]``
-    for each step that selects."""
-    Hkv = len(K)
-    g = num_q_heads // Hkv
-    states = new_states(Hkv, N_r, N_att)
-    for kvh in range(Hkv):
-        Kd = np.asarray(K[kvh], dtype=np.float64)
-        for t in range(t_end):
-            qg = np.asarray(Q_steps[t], dtype=np.float64)[kvh * g:(kvh + 1) * g] \
-                if states[kvh].needs_choice(t) else None
-            states[kvh].step(t, (lambda t_, idx_, qg=qg, Kd=Kd:
-                                 attention.select(qg, Kd[idx_], scale)[0]))
-    return states
-
-
 def random_states(num_kv_heads: int, N_r: int, N_att: int, t_end: int,
                   random_ints, mode: str = "diagonal", sinks: int = 0) -> List[alg1.HeadState]:
     """Selection states after steps ``0 .. t_end-1`` with the argmin replaced

@@ -87,15 +87,18 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->rows_max = static_cast<int>(rows_max);
   // Measured on MI355X: dense splits of ~24 KB for d = 64 (long ragged rows
   // balance better), ~96 KB for d = 128 and ~256 KB for the grouped-head
-  // tile (fewer partials to merge).  Sparse-mode splits of ~96 KB for every
-  // tile: against ~48 KB, fewer workgroups rebuild the same window ranking
-  // and fewer partials are merged (7-15% on layers of 16 or more requests at
-  // d = 128, no change below).  The fused step caps a split at
-  // kMaxFusedSplit rows.
+  // tile (fewer partials to merge).  Sparse-mode splits of ~192 KB on the
+  // vector-ALU tile, so a Janus-like request (256 prompt rows and 29 kept
+  // ones) is one split: no partials, no combine kernel, and the selection
+  // stays in the decode kernel (8% faster per layer than two splits, and
+  // faster on nearly every cell of the Janus-shaped sweep with 16 or more
+  // requests); ~96 KB on the MFMA tile.  The fused step caps a split at
+  // max_fused_split rows.
   const int dense_kb = d->MF ? kSplitKbDenseMfma : (d->D == 64 ? kSplitKbDense64 : kSplitKbDense128);
-  const int64_t split_bytes = (sparse ? kSplitKbSparse : dense_kb) * int64_t(1024);
+  const int sparse_kb = d->MF ? kSplitKbSparseMfma : kSplitKbSparse;
+  const int64_t split_bytes = (sparse ? sparse_kb : dense_kb) * int64_t(1024);
   int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
-  if (sparse) c_target = std::min<int64_t>(c_target, kMaxFusedSplit);
+  if (sparse) c_target = std::min<int64_t>(c_target, max_fused_split(d->MF));
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
   if (pairs * S < kMinWorkgroups) {
     const int64_t want = (kMinWorkgroups + pairs - 1) / pairs;

@@ -382,7 +382,7 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
           if (a.wlog)
             a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + lr) * a.plan_cap + (r - a.Lp)] =
                 logit;
-          if constexpr (FUSED) wls[lr * kMaxFusedSplit + (r - a.Lp - w0)] = logit;
+          if constexpr (FUSED) wls[lr * kMaxFusedSplitMfma + (r - a.Lp - w0)] = logit;
         }
       }
   }
@@ -472,7 +472,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   constexpr int NK = D / 32;       // MFMA k-steps per 16 rows (MF only)
   static_assert(T <= 64, "one kept position per lane");
   static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
-  constexpr int KS = FUSED ? kMaxFusedSplit : 1;
+  constexpr int KS = FUSED ? max_fused_split(MF) : 1;
   // The per-wave partial results (red) and, in the MFMA tile, the per-wave
   // V tiles share one LDS block: the V tiles are dead once every wave has
   // left the tile loop.

@@ -37,7 +37,10 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 // launch configuration and workspace size depend only on its parameters and
 // shape.  A tuning build may override any of them with -D.
 #ifndef DSA_TUNE_SPLIT_KB
-#define DSA_TUNE_SPLIT_KB 96  // K+V bytes per split workgroup, sparse modes
+#define DSA_TUNE_SPLIT_KB 192  // K+V bytes per split workgroup, sparse modes, vector-ALU tile
+#endif
+#ifndef DSA_TUNE_SPLIT_KB_MFMA
+#define DSA_TUNE_SPLIT_KB_MFMA 96  // the same for the grouped-head MFMA tile
 #endif
 #ifndef DSA_TUNE_SPLIT_KB_DENSE_64
 #define DSA_TUNE_SPLIT_KB_DENSE_64 24  // dense mode, d = 64, one query head per KV head
@@ -52,7 +55,11 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_MIN_WGS 512  // split further while a launch has fewer workgroups
 #endif
 #ifndef DSA_TUNE_MAX_FUSED_SPLIT
-#define DSA_TUNE_MAX_FUSED_SPLIT 256  // rows per sparse-mode split (the fused step keeps them in LDS)
+#define DSA_TUNE_MAX_FUSED_SPLIT 512  // most rows of a sparse-mode split (the fused step keeps
+                                      // their logits and positions in LDS), vector-ALU tile
+#endif
+#ifndef DSA_TUNE_MAX_FUSED_SPLIT_MFMA
+#define DSA_TUNE_MAX_FUSED_SPLIT_MFMA 256  // the same for the MFMA tile (its V tiles also use LDS)
 #endif
 #ifndef DSA_TUNE_UNROLL
 #define DSA_TUNE_UNROLL 0  // loads in flight per wave (2, 4 or 8); 0: by group size
@@ -65,12 +72,17 @@ constexpr int kWaves = 4;          // waves per workgroup in every kernel
 constexpr int kBlock = 64 * kWaves;
 constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
 constexpr int kMaxFusedSplit = DSA_TUNE_MAX_FUSED_SPLIT;
+constexpr int kMaxFusedSplitMfma = DSA_TUNE_MAX_FUSED_SPLIT_MFMA;
 constexpr int kSplitKbSparse = DSA_TUNE_SPLIT_KB;
+constexpr int kSplitKbSparseMfma = DSA_TUNE_SPLIT_KB_MFMA;
 constexpr int kSplitKbDense64 = DSA_TUNE_SPLIT_KB_DENSE_64;
 constexpr int kSplitKbDense128 = DSA_TUNE_SPLIT_KB_DENSE_128;
 constexpr int kSplitKbDenseMfma = DSA_TUNE_SPLIT_KB_DENSE_MFMA;
 constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
 static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
+static_assert(kMaxFusedSplitMfma % 64 == 0 && kMaxFusedSplitMfma <= 1024, "fused split rows");
+// Rows of one sparse-mode split at most, by tile.
+constexpr int max_fused_split(bool mfma) { return mfma ? kMaxFusedSplitMfma : kMaxFusedSplit; }
 
 // Grouped query heads take the MFMA tile (q.K^T and P.V on matrix cores).
 constexpr bool uses_mfma_tile(int G) { return G >= 2 && !DSA_TUNE_VALU_GQA; }

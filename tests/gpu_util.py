@@ -11,6 +11,7 @@ import numpy as np
 import torch
 
 from oracle import alg1
+from oracle.tieband import dot_band, logit_band, within_tie_band  # noqa: F401
 from paper_2609_19702_amd import binding as B
 
 DEV = "cuda"
@@ -76,40 +77,100 @@ def request_arrays(kv, b, Lp):
     return k[:, :Lp], v[:, :Lp], k[:, Lp:], v[:, Lp:]
 
 
-def dot_band(q, keys, scale):
-    """Forward-error bound of an fp32 dot product of length d, per key:
-    gamma_d * scale * sum_i |q_i k_i| with gamma_d = d u / (1 - d u)."""
-    d = q.shape[-1]
-    u = 2.0 ** -24
-    gamma = d * u / (1 - d * u)
-    return gamma * scale * (np.abs(keys) @ np.abs(q))
+def check_layer_vs_oracle(p, s, q, arrays, ts, states, plan_buf, out, state_after=None,
+                          logits=None, scale=None):
+    """One layer step of the library against the oracle's step from the same
+    selection states: kept sets bit for bit, every query head's output
+    within ``TOL``, the window logits (when given) within their fp32 bound,
+    and every phase-2 pick the library stored equal to the oracle's argmin
+    or inside the certified tie band (the oracle then adopts it).
+
+    ``arrays[b]`` holds request b's ``(Kp, Vp, K, V)`` as fp64 values of the
+    cache (dequantized for fp8); ``states[b]`` its per-KV-head oracle
+    states before the step (not modified).  Returns the number of near-tie
+    picks adopted."""
+    import copy
+    from oracle import step as ostep
+    mode = {B.MODE_DENSE: "dense", B.MODE_DIAGONAL: "diagonal",
+            B.MODE_WINDOW: "streaming"}[p.mode]
+    if p.mode == B.MODE_DIAGONAL and p.sinks:
+        mode = "diagonal_sink"
+    scale = 1.0 / math.sqrt(s.head_dim) if scale is None else scale
+    Hkv, g = s.num_kv_heads, s.num_q_heads // s.num_kv_heads
+    sparse = p.mode != B.MODE_DENSE
+    if sparse:
+        cnt, flg, idx = (x.cpu().numpy() for x in B.plan_views(p, s, plan_buf))
+    if state_after is not None:
+        scnt, sflg, soff = offsets_from_buffer(p, s, state_after)
+        assert not sflg.any()
+    o = out.double().cpu().numpy()
+    qn = q.double().cpu().numpy()
+    wl = None if logits is None else logits.view(s.batch, s.num_q_heads, -1).cpu().numpy()
+    forced = 0
+    for b, t in enumerate(ts):
+        if t < 0:
+            assert not o[b].any()
+            continue
+        Kp, Vp, K, V = arrays[b]
+
+        def decide(kvh, t_, idx_, j_ref, sigma, b=b):
+            nonlocal forced
+            if state_after is None:
+                return j_ref
+            pair = b * Hkv + kvh
+            k = t_ - (p.n_att - 1)
+            assert scnt[pair] == k + 1, (b, kvh, t_, scnt[pair])
+            j_gpu = idx_.index(t_ - int(soff[pair, k]))
+            if j_gpu != j_ref:
+                qg = qn[b][kvh * g:(kvh + 1) * g]
+                assert within_tie_band(qg, K[kvh][idx_], scale, j_gpu, j_ref), (b, kvh, t_)
+                forced += 1
+            return j_gpu
+
+        st = copy.deepcopy(states[b]) if states is not None and sparse else None
+        res = ostep.request_step(t, qn[b], Kp, Vp, K, V, scale, mode, st, decide, p.sinks)
+        for h in range(Hkv):
+            pair = b * Hkv + h
+            if sparse:
+                assert flg[pair] == 0, (b, h, flg[pair])
+                assert idx[pair, :cnt[pair]].tolist() == res.heads[h].idx, (b, h, t)
+                if wl is not None:
+                    kept = res.heads[h].idx
+                    for i in range(g):
+                        ref = res.heads[h].window_logits[i]
+                        band = logit_band(qn[b][h * g + i], K[h][kept], scale) + 1e-7
+                        got = wl[b, h * g + i, :len(kept)]
+                        assert (np.abs(got - ref) <= band).all(), (b, h, i)
+            for i in range(g):
+                e = rel_err(o[b, h * g + i], res.out[h * g + i])
+                assert e <= TOL, (b, h * g + i, e)
+    return forced
 
 
-def within_tie_band(q_group, window_keys, scale, j_gpu, j_ref) -> bool:
-    """Is the GPU's argmin ``j_gpu`` as good as the oracle's ``j_ref`` up to
-    the rounding the fp32 path may commit?
+def c_replay_states(N_r, N_att, L, ts, Hkv, rng, threads=8):
+    """Algorithm 1 states of every (request, KV head) before step ``ts[b]``,
+    each drawn by the C oracle's literal replay with random choices (fast
+    enough for windows of tens of thousands of positions).  Returns
+    ``(states, kept)``: ``states[b][h]`` an ``oracle.alg1.HeadState`` equal
+    to the literal state after steps ``0 .. t-1``, and ``kept[b][h]`` the
+    positions step ``t`` attends."""
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import coracle
+    jobs = [(b, h, max(t, 0), [rng.randrange(1 << 40) for _ in range(N_r)])
+            for b, t in enumerate(ts) for h in range(Hkv)]
 
-    Group size 1: the GPU compares fp32 logits, each within ``dot_band`` of
-    the exact logit (plus the rounding of the scale multiply), so any pick
-    whose exact logit exceeds the minimum by at most the two bands is valid.
-    Larger groups: a logit error of at most ``beta_h`` changes each window
-    softmax weight by a factor within ``exp(+-2 beta_h)``; with the fp32
-    exp/divide rounding this bounds the error of the summed score."""
-    q_group = np.atleast_2d(np.asarray(q_group, np.float64))
-    keys = np.asarray(window_keys, np.float64)
-    if j_gpu == j_ref:
-        return True
-    if q_group.shape[0] == 1:
-        s = scale * keys @ q_group[0]
-        band = dot_band(q_group[0], keys, scale) + 2.0 ** -23 * np.abs(s)
-        return s[j_gpu] - s[j_ref] <= band[j_gpu] + band[j_ref]
-    sig = np.zeros(len(keys))
-    slack = 1e-7 * q_group.shape[0]
-    for q in q_group:
-        s = scale * keys @ q
-        w = np.exp(s - s.max())
-        w /= w.sum()
-        sig += w
-        beta = (dot_band(q, keys, scale) + 2.0 ** -23 * np.abs(s)).max()
-        slack += (w[j_gpu] + w[j_ref]) * (2 * beta + 8e-6)
-    return sig[j_gpu] - sig[j_ref] <= slack
+    def one(job):
+        b, h, t, rand = job
+        skip_used, kept = coracle.alg1_replay(N_r, N_att, L, t, rand)
+        st = alg1.HeadState(N_r, N_att)
+        # the list before step t's shift, and the positions evicted before t
+        st.skip_idx = [j - 1 for j in skip_used] if st.phase(t) >= 2 else list(skip_used)
+        st.evicted = set(range(0, max(0, t - N_r)))
+        return b, h, st, kept
+
+    states = [[None] * Hkv for _ in ts]
+    kept = [[None] * Hkv for _ in ts]
+    with ThreadPoolExecutor(threads) as ex:
+        for b, h, st, kp in ex.map(one, jobs):
+            states[b][h], kept[b][h] = st, kp
+    return states, kept

@@ -178,7 +178,7 @@ def test_struct_layouts_match_the_header(tmp_path):
 BENCH_CONFIGS = {
     ("llamagen_xl", 1): (192, 1, 1280, 3, 8),
     ("llamagen_xl", 0): (128, 6, 7680, 3, 8),
-    ("janus_pro_7b", 1): (160, 2, 8192, 4, 8),
+    ("janus_pro_7b", 1): (288, 1, 4096, 4, 8),
     ("janus_pro_7b", 0): (192, 5, 20480, 4, 8),
     ("emu3_8b_gqa", 1): (160, 3, 768, 4, 100),
     ("emu3_8b_gqa", 0): (512, 9, 2304, 4, 100),

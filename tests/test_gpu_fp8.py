@@ -23,7 +23,7 @@ from oracle import fp8 as ofp8
 from oracle import step as ostep
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import DEV, TOL, dot_band, rel_err, say, states_to_buffer
+from tests.gpu_util import DEV, TOL, check_layer_vs_oracle, dot_band, rel_err, say, states_to_buffer
 
 pytestmark = pytest.mark.gpu
 
@@ -213,8 +213,12 @@ def test_fp8_ring_equals_linear():
         B.decode_step(p, s, q, k, v, lay, pos, st, bufs.plan, 0.1, bufs.out, bufs.logits,
                       bufs.workspace)
         torch.cuda.synchronize()
-        res.append((bufs.out.clone(), st.clone()))
+        res.append((bufs.out.clone(), st.clone(), bufs.plan.clone(), bufs.logits.clone()))
     assert torch.equal(res[0][0], res[1][0]) and torch.equal(res[0][1], res[1][1])
+    # the ring's results against the oracle on the dequantized cache
+    arrays = [fp8_request_arrays(kv, b, Lp, Hkv) for b in range(Bn)]
+    o1, s1, p1, l1 = res[1]
+    assert check_layer_vs_oracle(p, s, q, arrays, ts, states, p1, o1, s1, l1, scale=0.1) <= 1
 
 
 def test_fp8_argument_errors():

@@ -1,8 +1,12 @@
-"""Ring-buffer KV (physical eviction): a cache of L_p + R rows per (request,
-KV head) in which decode position j lives in slot j mod R must give exactly
-the outputs, plans and selection states of the linear cache.  Only the live
-window of each request is copied into the ring; every other slot holds a
-large decoy value, so a read of an evicted row would show."""
+"""Ring-buffer KV (physical eviction, section 4 "Cost analysis"): a cache of
+L_p + R rows per (request, KV head) in which decode position j lives in slot
+j mod R.  Its plans, outputs, window logits and stored selections are
+checked against the oracle's step from the same selection states (kept sets
+bit for bit, outputs within the tolerance, picks equal to the oracle's
+argmin or inside the certified tie band), and must equal the linear cache's
+results bit for bit.  Only the live window of each request is copied into
+the ring; every other slot holds a large decoy value, so a read of an
+evicted row would show."""
 
 import random
 
@@ -13,7 +17,7 @@ import torch
 from oracle import step as ostep
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import DEV, say, states_to_buffer
+from tests.gpu_util import DEV, check_layer_vs_oracle, request_arrays, say, states_to_buffer
 
 pytestmark = pytest.mark.gpu
 
@@ -73,9 +77,12 @@ def test_ring_equals_linear(case, fused):
                                bufs.workspace)
             B.select(p, s, pos, bufs.plan, bufs.logits, st)
         torch.cuda.synchronize()
-        results.append((bufs.out.clone(), st.clone(), bufs.plan.clone()))
-    (o0, s0, p0), (o1, s1, p1) = results
+        results.append((bufs.out.clone(), st.clone(), bufs.plan.clone(), bufs.logits.clone()))
+    (o0, s0, p0, _), (o1, s1, p1, l1) = results
     assert torch.isfinite(o1).all()
+    arrays = [request_arrays(kv, b, Lp) for b in range(Bn)]
+    forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, p1, o1, s1, l1, scale=0.125)
+    assert forced <= 1
     assert torch.equal(o0, o1)
     assert torch.equal(s0, s1)
     assert torch.equal(p0, p1)

@@ -9,8 +9,8 @@ window (window mode with S sinks, or none).
   outputs within the tolerance, phase-2 choices equal to the oracle's argmin
   or inside the fp32 rounding band of it; the fused step reproduces the
   three separate calls bit for bit at every step;
-* the ring layout with pinned sink rows gives the linear cache's results
-  bit for bit;
+* the ring layout with pinned sink rows gives the oracle's results, and the
+  linear cache's bit for bit;
 * window mode needs no selection state or logits buffer."""
 
 import copy
@@ -24,7 +24,8 @@ import torch
 from oracle import step as ostep
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import DEV, TOL, offsets_from_buffer, rel_err, say, states_to_buffer, within_tie_band
+from tests.gpu_util import (DEV, TOL, check_layer_vs_oracle, offsets_from_buffer, rel_err, request_arrays,
+                            say, states_to_buffer, within_tie_band)
 
 pytestmark = pytest.mark.gpu
 
@@ -214,9 +215,13 @@ def test_sink_ring_equals_linear(case, fused):
                                bufs.workspace)
             B.select(p, s, pos, bufs.plan, bufs.logits, st)
         torch.cuda.synchronize()
-        results.append((bufs.out.clone(), None if st is None else st.clone(), bufs.plan.clone()))
-    (o0, s0, p0), (o1, s1, p1) = results
+        results.append((bufs.out.clone(), None if st is None else st.clone(), bufs.plan.clone(),
+                        bufs.logits.clone()))
+    (o0, s0, p0, _), (o1, s1, p1, l1) = results
     assert torch.isfinite(o1).all()
+    arrays = [request_arrays(kv, b, Lp) for b in range(Bn)]
+    forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, p1, o1, s1, l1, scale=0.125)
+    assert forced <= 1
     assert torch.equal(o0, o1)
     assert s0 is None or torch.equal(s0, s1)
     assert torch.equal(p0, p1)
