@@ -377,6 +377,31 @@ DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s
                                          hipEvent_t decode_stop, hipStream_t stream);
 
 /*
+ * dsa_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same step with the same results, bit for bit, but without a workspace
+ * argument.  The split partials go to a buffer of
+ * DSA_NOALLOC_SCRATCH_BYTES bytes inside the library, one per GPU, held
+ * until the process ends.  The call allocates nothing and needs no memset.
+ *   arguments   as dsa_decode_step (the caller still passes the state, plan,
+ *               window logits and output buffers)
+ * Every call on one GPU shares that GPU's buffer: two calls on one GPU whose
+ * execution overlaps (different streams, no ordering between them) race and
+ * give undefined results; calls ordered on one stream are safe.
+ * Errors: as dsa_decode_step; WORKSPACE when the call would need more
+ * partials than the buffer holds (dsa_workspace_bytes() >
+ * DSA_NOALLOC_SCRATCH_BYTES: use dsa_decode_step with a caller workspace);
+ * HIP when the buffer's device address cannot be obtained.
+ */
+#define DSA_NOALLOC_SCRATCH_BYTES (16u << 20)
+DSA_API dsa_status dsa_decode_step_noalloc(const dsa_params* p, const dsa_shape* s,
+                                           const void* d_q, const void* d_k, const void* d_v,
+                                           const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                           void* d_state, void* d_plan, size_t plan_bytes,
+                                           float sm_scale, float* d_out, float* d_window_logits,
+                                           hipStream_t stream);
+
+/*
  * Phase-2 selection of Algorithm 1: for every request with
  * N_att - 1 <= t_b <= N_r + S - 2 and every KV head h, compute
  *   w_q = softmax(window logits of query head q)   over the kept window

@@ -106,8 +106,12 @@ SIGNATURES = {
     "dsa_decode_step_timed": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP, _VP,
                                           _VP, C.c_size_t, C.c_float, _VP, _VP, _VP, C.c_size_t,
                                           _VP, _VP, _VP]),
+    "dsa_decode_step_noalloc": (C.c_int32, [_P, _S, _VP, _VP, _VP, C.POINTER(KVLayout), _VP, _VP,
+                                            _VP, C.c_size_t, C.c_float, _VP, _VP, _VP]),
     "dsa_select": (C.c_int32, [_P, _S, _VP, _VP, _VP, _VP, _VP]),
 }
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # DSA_NOALLOC_SCRATCH_BYTES
 
 _lib = None
 
@@ -274,6 +278,18 @@ def decode_step(p, s, q, k, v, layout: KVLayout, decode_pos, state, plan_buf, sm
     else:
         _check(lib().dsa_decode_step_timed(*args, events[0].cuda_event, events[1].cuda_event,
                                            _stream(stream)), "dsa_decode_step_timed")
+
+
+def decode_step_noalloc(p, s, q, k, v, layout: KVLayout, decode_pos, state, plan_buf, sm_scale,
+                        out, window_logits, stream=None):
+    """``decode_step`` without a workspace: the split partials live in the
+    library's own per-GPU buffer (for callers that cannot allocate)."""
+    pb = 0 if plan_buf is None else plan_buf.numel() * plan_buf.element_size()
+    _check(lib().dsa_decode_step_noalloc(C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v),
+                                         C.byref(layout), _ptr(decode_pos), _ptr(state),
+                                         _ptr(plan_buf), pb, float(sm_scale), _ptr(out),
+                                         _ptr(window_logits), _stream(stream)),
+           "dsa_decode_step_noalloc")
 
 
 def timing_events():

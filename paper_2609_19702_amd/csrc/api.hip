@@ -1,6 +1,7 @@
 // Host side of the C ABI: argument validation, buffer layouts, the split
 // configuration of the decode kernel, and the extern "C" entry points.
 #include <cmath>
+#include <mutex>
 
 #include "internal.h"
 
@@ -428,6 +429,61 @@ DSA_API dsa_status dsa_decode_step_timed(const dsa_params* p, const dsa_shape* s
   return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
                      d_window_logits, d_ws, ws_bytes, decode_start, decode_stop, stream, true,
                      d_state, plan_bytes);
+}
+
+}  // extern "C"
+
+// Split partials of dsa_decode_step_noalloc: a file-scope device array, one
+// copy per GPU, held until the process ends.  Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the
+// symbol); it uses the device address hipGetSymbolAddress returns on each
+// GPU, looked up once per device on the first call made with that device
+// current.  Nothing needs clearing between calls: each split writes its own
+// partial before the combine reads it, and the combine reads only splits
+// that exist.
+static __device__ __align__(256) unsigned char scratch[DSA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's copy of `scratch`, or nullptr.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+DSA_API dsa_status dsa_decode_step_noalloc(const dsa_params* p, const dsa_shape* s,
+                                           const void* d_q, const void* d_k, const void* d_v,
+                                           const dsa_kv_layout* kv, const int32_t* d_decode_pos,
+                                           void* d_state, void* d_plan, size_t plan_bytes,
+                                           float sm_scale, float* d_out, float* d_window_logits,
+                                           hipStream_t stream) {
+  Derived d;
+  dsa_status st = dsa::derive(p, s, &d);
+  if (st != DSA_OK) return st;
+  if (d.ws_bytes > DSA_NOALLOC_SCRATCH_BYTES) return DSA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (d.ws_bytes) {
+    ws = scratch_on_current_device();
+    if (!ws) return DSA_ERR_HIP;
+  }
+  return decode_impl(p, s, d_q, d_k, d_v, kv, d_decode_pos, d_plan, sm_scale, d_out,
+                     d_window_logits, ws, d.ws_bytes ? DSA_NOALLOC_SCRATCH_BYTES : 0, nullptr,
+                     nullptr, stream, true, d_state, plan_bytes);
 }
 
 DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int32_t* d_decode_pos,
