@@ -29,8 +29,9 @@ the last kernel of the call (the combine, when requests are split), over
 those steps waits behind a spin kernel until the host has issued all of it,
 so its layers run back to back as in the timed graph replays (``--eager``
 times launches as issued, without the spin).  ``cpu_baseline`` times the fp64 CPU oracle on a bounded sample
-of the same workload on one core, and (``all_cores``) on every host core as a
-pool of single-threaded processes (``--no-cpu-baseline`` skips both).
+of the same workload: the C oracle on the host's cores (OpenMP over KV
+heads, ``value``) and on one thread, and the Python oracle on one thread
+(``--no-cpu-baseline`` skips them).
 """
 
 from __future__ import annotations
@@ -62,7 +63,8 @@ def parse():
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--only", default=None,
-                    choices=["fused", "separate", "dense", "diag_sink4", "streaming", "fp8_kv"],
+                    choices=["fused", "separate", "dense", "diag_sink4", "streaming", "fp8_kv",
+                             "ring"],
                     help="time one step variant only (shorter profiler runs)")
     ap.add_argument("--sweep", action="store_true",
                     help="time the Janus-shaped sweep (grid x batch x window, diagonal and dense) "
@@ -106,33 +108,54 @@ def traffic_for(workload, src_hash):
     return ent.get("hbm_bytes_per_launch")
 
 
-def oracle_units(bt):
-    """A bounded sample of the workload for the CPU oracle: six requests of
-    layer 0 spread over the decode positions, with a valid selection state
-    each (fp64 numpy arrays)."""
-    import numpy as np  # noqa: F401
+def oracle_units(bt, n=16):
+    """A bounded sample of the workload for the CPU oracle: ``n`` requests of
+    layer 0 spread over the decode positions, each with the Algorithm 1
+    states its KV heads have before that position (replayed by the C
+    oracle with seeded random choices), as contiguous fp64 numpy arrays."""
+    import numpy as np
     import torch
-    from oracle import step as ostep
+    from oracle import coracle
     from paper_2609_19702_amd import synth
     w, L = bt.w, bt.layers[0]
     order = sorted(range(w.batch), key=lambda b: bt.pos_host[b])
-    pick = [order[i * (len(order) - 1) // 5] for i in range(6)]
+    n = min(n, w.batch)
+    pick = [order[i * (len(order) - 1) // max(n - 1, 1)] for i in range(n)]
     units = []
     qn = L.q.to(torch.float64).cpu().numpy()
+    N_r, N_att = bt.p.window, bt.p.n_att
+    Lp = w.prompt_len
     for b in pick:
         t = bt.pos_host[b]
-        k = L.kv.k[b, :, :w.prompt_len + t + 1].to(torch.float64).cpu().numpy()
-        v = L.kv.v[b, :, :w.prompt_len + t + 1].to(torch.float64).cpu().numpy()
-        ints = synth.random_ints(w, 0, w.num_kv_heads * w.window, sub=b).tolist()
-        st = ostep.random_states(w.num_kv_heads, bt.p.window, bt.p.n_att, t, ints)
-        units.append((t, qn[b], k[:, :w.prompt_len], v[:, :w.prompt_len],
-                      k[:, w.prompt_len:], v[:, w.prompt_len:], st))
+        # each slice becomes one dense fp64 array in a single conversion
+        arr = [x[b, :, r0:r1].to(torch.float64).contiguous().cpu().numpy()
+               for x in (L.kv.k, L.kv.v) for (r0, r1) in ((0, Lp), (Lp, Lp + t + 1))]
+        ints = synth.random_ints(w, 0, w.num_kv_heads * N_r, sub=b).tolist()
+        heads = [coracle.replay_head(N_r, N_att, w.decode_len, t, ints[h * N_r:(h + 1) * N_r])[0]
+                 for h in range(w.num_kv_heads)]
+        units.append((t, np.ascontiguousarray(qn[b]), arr[0], arr[2], arr[1], arr[3], heads,
+                      coracle.States.from_heads(heads, w.decode_len)))
     return pick, units
 
 
-def oracle_loop(units, scale, seconds):
-    """Run the oracle's decode step over ``units`` until ``seconds`` of wall
-    time are spent on it, numpy on one thread; returns (steps, seconds)."""
+def c_oracle_loop(units, scale, seconds, threads):
+    """The C oracle's decode step (attention of every head + selection, fp64)
+    over ``units`` until ``seconds`` are spent inside it; returns
+    (steps, seconds).  State copies are made outside the timed calls."""
+    from oracle import coracle
+    done, spent = 0, 0.0
+    while spent < seconds:
+        for (t, q, Kp, Vp, K, V, _, cstates) in units:
+            st = cstates.copy()
+            t0 = time.perf_counter()
+            coracle.request_step(t, q, Kp, Vp, K, V, scale, "diagonal", st, threads=threads)
+            spent += time.perf_counter() - t0
+            done += 1
+    return done, spent
+
+
+def py_oracle_loop(units, scale, seconds):
+    """The Python (numpy) oracle's decode step over ``units``, one thread."""
     from oracle import step as ostep
     try:
         from threadpoolctl import threadpool_limits
@@ -142,52 +165,45 @@ def oracle_loop(units, scale, seconds):
     done, spent = 0, 0.0
     try:
         while spent < seconds:
-            for (t, q, Kp, Vp, K, V, st) in units:
-                st2 = copy.deepcopy(st)
+            for (t, q, Kp, Vp, K, V, heads, _) in units:
+                st2 = copy.deepcopy(heads)
                 t0 = time.perf_counter()
                 ostep.request_step(t, q, Kp, Vp, K, V, scale, "diagonal", st2)
                 spent += time.perf_counter() - t0
                 done += 1
+                if spent >= seconds:
+                    break
     finally:
         if ctx is not None:
             ctx.__exit__(None, None, None)
     return done, spent
 
 
-def _oracle_worker(args):
-    units, scale, seconds = args
-    return oracle_loop(units, scale, seconds)
-
-
 def cpu_baseline(bt, seconds):
-    """The fp64 oracle on a bounded sample (``oracle_units``), each decode
-    step repeated until about ``seconds`` of CPU time is spent, on one core;
-    then the same sample on every host core (a process pool of one numpy
-    thread per process, at most 16), which adds ``all_cores``."""
-    import multiprocessing as mp
+    """The fp64 CPU oracle on a bounded sample (``oracle_units``): the C
+    oracle with OpenMP over KV heads on the host's cores (``value``), the
+    same on one thread, and the Python oracle on one thread, each decode
+    step repeated until about ``seconds`` (a third of it for the Python
+    oracle) is spent."""
     w = bt.w
     pick, units = oracle_units(bt)
-    done, spent = oracle_loop(units, bt.scale, seconds)
-    tok_s = done / spent / len(bt.layers)
-    res = {"value": tok_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-           "sample": (f"{len(units)} requests of layer 0 (positions "
-                      f"{[bt.pos_host[b] for b in pick]}), one decode step each (attention "
-                      f"for all {w.num_q_heads} heads + selection), repeated {done} times in "
-                      f"{spent:.1f} s; tokens/s = steps / s / {len(bt.layers)} layers")}
     cores = max(1, min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity")
                        else (os.cpu_count() or 1)))
-    if cores > 1:
-        per = max(2.0, seconds / 2)
-        t0 = time.perf_counter()
-        with mp.get_context("spawn").Pool(cores) as pool:
-            outs = pool.map(_oracle_worker, [(units, bt.scale, per)] * cores)
-        wall = time.perf_counter() - t0
-        steps = sum(d for d, _ in outs)
-        busy = max(sp for _, sp in outs)
-        res["all_cores"] = {"value": steps / busy / len(bt.layers), "cores": cores,
-                            "steps": steps, "seconds_per_worker": busy,
-                            "wall_s_with_startup": wall}
-    return res
+    nl = len(bt.layers)
+    d_all, s_all = c_oracle_loop(units, bt.scale, seconds / 2, cores)
+    d_one, s_one = c_oracle_loop(units, bt.scale, seconds / 2, 1)
+    d_py, s_py = py_oracle_loop(units, bt.scale, seconds / 3)
+    pos = sorted(bt.pos_host[b] for b in pick)
+    return {"value": d_all / s_all / nl, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"C oracle (fp64, OpenMP over the {w.num_kv_heads} KV heads): one decode "
+                       f"step (attention of all {w.num_q_heads} heads + phase-2 selection) of "
+                       f"{len(units)} requests of layer 0 at positions {pos[0]}..{pos[-1]}, "
+                       f"repeated {d_all} times in {s_all:.1f} s; tokens/s = steps / s / "
+                       f"{nl} layers"),
+            "one_thread": {"value": d_one / s_one / nl, "cores": 1, "steps": d_one,
+                           "seconds": s_one},
+            "python_oracle_one_thread": {"value": d_py / s_py / nl, "cores": 1, "steps": d_py,
+                                         "seconds": s_py}}
 
 
 VARIANTS = {}  # mode name -> workload.Variant, filled by main()
@@ -454,13 +470,15 @@ def main():
     bt = workload.make_batch(w)
     workload.build_histories(bt)
     modes = (args.only,) if args.only else ("fused", "separate", "dense", "diag_sink4", "streaming",
-                                             "fp8_kv")
+                                             "fp8_kv", "ring")
     if "diag_sink4" in modes:
         VARIANTS["diag_sink4"] = workload.make_variant(bt, "diag_sink4", B.MODE_DIAGONAL, 4)
     if "streaming" in modes:
         VARIANTS["streaming"] = workload.make_variant(bt, "streaming", B.MODE_WINDOW, 4)
     if "fp8_kv" in modes:
         VARIANTS["fp8_kv"] = workload.make_variant(bt, "fp8_kv", B.MODE_DIAGONAL, 0, fp8=True)
+    if "ring" in modes:
+        VARIANTS["ring"] = workload.make_ring_variant(bt)
     torch.cuda.synchronize()
     print(f"# setup {time.time() - t0:.1f}s: {w.name} layers={len(bt.layers)} batch={w.batch} "
           f"n_att={bt.p.n_att} window={bt.p.window}", file=sys.stderr, flush=True)
@@ -542,8 +560,10 @@ def main():
                 "decode_launch_gbps": bt.kv_bytes(False, 1 if m == "fp8_kv" else 2) / n_layers
                 / (statistics.fmean(launch[m]) * 1e-3) / 1e9,
                 "mode": {"diag_sink4": "diagonal, 4 sinks", "streaming": "window, 4 sinks",
-                         "fp8_kv": "diagonal, fp8 E4M3 KV with per-(request, KV head) scales"}[m]}
-            for m in ("diag_sink4", "streaming", "fp8_kv")
+                         "fp8_kv": "diagonal, fp8 E4M3 KV with per-(request, KV head) scales",
+                         "ring": "diagonal, ring cache of R = N_r decode slots (physical "
+                                 "eviction)"}[m]}
+            for m in ("diag_sink4", "streaming", "fp8_kv", "ring")
         },
         "speedup_vs_dense": ms_dense / ms_sparse,
         "ideal_speedup": bytes_dense / bytes_sparse,
@@ -562,6 +582,18 @@ def main():
         "cpu_baseline": base,
         "paper_context": PAPER_CONTEXT,
     }
+    if "ring" in VARIANTS:
+        ring = VARIANTS["ring"]
+        R = ring.ring_rows
+        row_bytes = w.num_kv_heads * w.head_dim * 2 * 2 * w.batch  # K and V, bf16, all requests
+        res["variants"]["ring"].update({
+            "ring_rows": R,
+            "kv_resident_bytes_per_layer": (w.prompt_len + R) * row_bytes,
+            "linear_kv_resident_bytes_per_layer": (w.prompt_len + w.decode_len) * row_bytes,
+            "step_vs_linear": ms["ring"] / ms_sparse,
+            "outputs_match_linear": all(torch.equal(L.bufs.out, bf.out)
+                                        for L, bf in zip(bt.layers, ring.bufs)),
+        })
     print(json.dumps(res), flush=True)
 
 

@@ -80,6 +80,22 @@ def alg1_replay(N_r: int, N_att: int, L: int, t_end: int,
     return skip[:ns[0]].tolist(), idx[:ni[0]].tolist()
 
 
+def replay_head(N_r: int, N_att: int, L: int, t: int, rand: Sequence[int]):
+    """Algorithm 1 state of one head before step ``t`` (after steps
+    ``0 .. t-1`` with the k-th choice ``rand[k] mod |idx|``) as an
+    ``oracle.alg1.HeadState``, plus the positions step ``t`` attends.  The
+    C replay also runs step ``t`` (without a choice); the state before it is
+    its skip list one position back along each diagonal when step ``t``
+    shifted it (phase 2 or 3), and the positions evicted at steps before
+    ``t`` (``t' - N_r`` for ``N_r <= t' < t``)."""
+    from . import alg1
+    skip_used, kept = alg1_replay(N_r, N_att, L, t, rand)
+    st = alg1.HeadState(N_r, N_att)
+    st.skip_idx = [j - 1 for j in skip_used] if st.phase(t) >= 2 else list(skip_used)
+    st.evicted = set(range(0, max(0, t - N_r)))
+    return st, kept
+
+
 @dataclass
 class States:
     """Algorithm 1 states of the KV heads of one request, in the C oracle's

@@ -154,6 +154,49 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
+def _nbytes(x) -> int:
+    return x.numel() * x.element_size()
+
+
+def _need(x, name, dtype=None, min_bytes=0, contiguous=True):
+    """Argument checks before a device call (tensors only; raw integer
+    pointers pass through unchecked): on the GPU, of the expected element
+    type, dense where the library assumes it, and at least ``min_bytes``
+    long.  A mismatch raises ``ValueError`` instead of letting the kernels
+    read or write outside the tensor."""
+    if x is None or isinstance(x, int):
+        return
+    if not x.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and x.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError(f"{name} must be {dtype}, got {x.dtype}")
+    if contiguous and not x.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if _nbytes(x) < min_bytes:
+        raise ValueError(f"{name} holds {_nbytes(x)} bytes, needs {min_bytes}")
+
+
+_KV_DTYPES = (torch.bfloat16, torch.uint8, torch.float8_e4m3fn)
+
+
+def _check_decode_args(p, s, q, k, v, layout, decode_pos, out, window_logits):
+    B_, Hq, Hkv, d = s.batch, s.num_q_heads, s.num_kv_heads, s.head_dim
+    _need(q, "q", torch.bfloat16, B_ * Hq * d * 2)
+    _need(out, "out", torch.float32, B_ * Hq * d * 4)
+    _need(decode_pos, "decode_pos", torch.int32, B_ * 4)
+    _need(window_logits, "window_logits", torch.float32, window_logits_count(p, s) * 4)
+    for x, name in ((k, "k"), (v, "v")):
+        _need(x, name, _KV_DTYPES, contiguous=False)
+    if isinstance(k, torch.Tensor) and isinstance(v, torch.Tensor):
+        if k.dtype != v.dtype or k.shape != v.shape or k.stride() != v.stride():
+            raise ValueError("k and v must share element type, shape and strides")
+        if k.dim() == 4 and layout.d_row_base is None:
+            rows_needed = p.prompt_len + (layout.ring_rows if layout.ring_rows else 1)
+            if k.shape[0] < B_ or k.shape[1] < Hkv or k.shape[3] != d or k.shape[2] < rows_needed:
+                raise ValueError(f"cache of shape {tuple(k.shape)} does not hold {B_} requests x "
+                                 f"{Hkv} KV heads x {rows_needed}+ rows of {d} elements")
+
+
 # ---- host-only helpers ------------------------------------------------------
 
 def abi_version() -> int:
@@ -223,6 +266,8 @@ def state_reset(p, s, state, req_mask=None, stream=None):
 
 
 def plan(p, s, decode_pos, state, plan_buf, stream=None):
+    _need(decode_pos, "decode_pos", torch.int32, s.batch * 4)
+    _need(state, "state", None, state_bytes(p, s) if state_layout(p, s).cap else 0)
     _check(lib().dsa_plan(C.byref(p), C.byref(s), _ptr(decode_pos), _ptr(state), _ptr(plan_buf),
                           plan_buf.numel() * plan_buf.element_size(), _stream(stream)), "dsa_plan")
 
@@ -253,7 +298,11 @@ def kv_layout(k: torch.Tensor, row_base: Optional[torch.Tensor] = None,
 def decode_attention(p, s, q, k, v, layout: KVLayout, decode_pos, plan_buf, sm_scale, out,
                      window_logits=None, workspace=None, stream=None, events=None):
     """``events``: optional (start, stop) pair from ``timing_events()``; they
-    then receive the split-K kernel's own start and end timestamps."""
+    then receive the start of the split-K kernel and the end of the call's
+    last kernel."""
+    _check_decode_args(p, s, q, k, v, layout, decode_pos, out, window_logits)
+    if p.mode != MODE_DENSE:
+        _need(plan_buf, "plan", None, plan_bytes(p, s))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     args = (C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v), C.byref(layout), _ptr(decode_pos),
             _ptr(plan_buf), float(sm_scale), _ptr(out), _ptr(window_logits), _ptr(workspace),
@@ -268,6 +317,8 @@ def decode_attention(p, s, q, k, v, layout: KVLayout, decode_pos, plan_buf, sm_s
 def decode_step(p, s, q, k, v, layout: KVLayout, decode_pos, state, plan_buf, sm_scale, out,
                 window_logits, workspace=None, stream=None, events=None):
     """One fused decode step: plan + attention + selection in one pass."""
+    _check_decode_args(p, s, q, k, v, layout, decode_pos, out, window_logits)
+    _need(state, "state", None, state_bytes(p, s) if state_layout(p, s).cap else 0)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     pb = 0 if plan_buf is None else plan_buf.numel() * plan_buf.element_size()
     args = (C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v), C.byref(layout), _ptr(decode_pos),
@@ -284,6 +335,8 @@ def decode_step_noalloc(p, s, q, k, v, layout: KVLayout, decode_pos, state, plan
                         out, window_logits, stream=None):
     """``decode_step`` without a workspace: the split partials live in the
     library's own per-GPU buffer (for callers that cannot allocate)."""
+    _check_decode_args(p, s, q, k, v, layout, decode_pos, out, window_logits)
+    _need(state, "state", None, state_bytes(p, s) if state_layout(p, s).cap else 0)
     pb = 0 if plan_buf is None else plan_buf.numel() * plan_buf.element_size()
     _check(lib().dsa_decode_step_noalloc(C.byref(p), C.byref(s), _ptr(q), _ptr(k), _ptr(v),
                                          C.byref(layout), _ptr(decode_pos), _ptr(state),
@@ -302,6 +355,11 @@ def timing_events():
 
 
 def select(p, s, decode_pos, plan_buf, window_logits, state, stream=None):
+    if state_layout(p, s).cap:
+        _need(decode_pos, "decode_pos", torch.int32, s.batch * 4)
+        _need(plan_buf, "plan", None, plan_bytes(p, s))
+        _need(window_logits, "window_logits", torch.float32, window_logits_count(p, s) * 4)
+        _need(state, "state", None, state_bytes(p, s))
     _check(lib().dsa_select(C.byref(p), C.byref(s), _ptr(decode_pos), _ptr(plan_buf),
                             _ptr(window_logits), _ptr(state), _stream(stream)), "dsa_select")
 

@@ -79,16 +79,18 @@ def make_batch(w: synth.Workload, layers: Optional[int] = None, device="cuda",
 
 @dataclass
 class Variant:
-    """Another index-builder mode, or another KV element type, over the
-    batch's queries, with its own per-layer buffers (and caches, for fp8)."""
+    """Another index-builder mode, another KV element type or a ring-buffer
+    cache, over the batch's queries, with its own per-layer buffers (and
+    caches, for fp8 and the ring)."""
     name: str
     p: B.Params
     bufs: List[B.Buffers]
     kvs: Optional[List[synth.LayerKV]] = None
+    ring_rows: int = 0
 
 
-def kv_layout_of(kv: synth.LayerKV) -> B.KVLayout:
-    return B.kv_layout(kv.k, k_scale=kv.k_scale, v_scale=kv.v_scale)
+def kv_layout_of(kv: synth.LayerKV, ring_rows: int = 0) -> B.KVLayout:
+    return B.kv_layout(kv.k, ring_rows=ring_rows, k_scale=kv.k_scale, v_scale=kv.v_scale)
 
 
 def build_histories(bt: Batch, device="cuda", p: Optional[B.Params] = None,
@@ -132,6 +134,40 @@ def make_variant(bt: Batch, name: str, mode: int, sinks: int, device="cuda",
     return v
 
 
+def ring_cache(kv: synth.LayerKV, prompt_len: int, pos_host: List[int], R: int,
+               device="cuda") -> synth.LayerKV:
+    """The cache as a ring of ``R`` decode slots per (request, KV head)
+    (section 4, "Cost analysis": physical eviction): the prompt rows, then
+    decode position ``j`` of the live window ``[t - R + 1, t]`` in slot
+    ``j mod R``.  Slots no live position maps to keep a copy of the prompt's
+    first row; no step reads them."""
+    Bn, H, _, d = kv.k.shape
+    t = torch.tensor(pos_host, dtype=torch.int64, device=device).clamp_min(0)[:, None]
+    r = torch.arange(R, dtype=torch.int64, device=device)[None, :]
+    j = t - torch.remainder(t - r, R)                 # the live position stored in slot r
+    src = torch.where(j >= 0, prompt_len + j, torch.zeros_like(j))
+    src = src[:, None, :, None].expand(Bn, H, R, d)
+    out = []
+    for x in (kv.k, kv.v):
+        ring = torch.empty((Bn, H, prompt_len + R, d), dtype=x.dtype, device=device)
+        ring[:, :, :prompt_len] = x[:, :, :prompt_len]
+        ring[:, :, prompt_len:] = torch.gather(x, 2, src)
+        out.append(ring)
+    return synth.LayerKV(out[0], out[1], prompt_len + R, kv.k_scale, kv.v_scale)
+
+
+def make_ring_variant(bt: Batch, device="cuda") -> Variant:
+    """The batch's diagonal step over ring caches of ``R = N_r`` decode
+    slots, the least Algorithm 1 allows, starting from copies of the
+    batch's selection states."""
+    R = bt.p.window + bt.p.sinks
+    kvs = [ring_cache(L.kv, bt.w.prompt_len, bt.pos_host, R, device) for L in bt.layers]
+    bufs = [B.alloc_buffers(bt.p, bt.s, device) for _ in bt.layers]
+    for bf, L in zip(bufs, bt.layers):
+        bf.state.copy_(L.bufs.state)
+    return Variant("ring", bt.p, bufs, kvs, ring_rows=R)
+
+
 def sparse_layer(bt: Batch, L: Layer, timer=None):
     p, s = bt.p, bt.s
     B.plan(p, s, bt.pos, L.bufs.state, L.bufs.plan)
@@ -154,8 +190,8 @@ def dense_layer(bt: Batch, L: Layer, timer=None):
 def variant_layer(bt: Batch, v: Variant, i: int, timer=None):
     L, bf = bt.layers[i], v.bufs[i]
     kv = L.kv if v.kvs is None else v.kvs[i]
-    B.decode_step(v.p, bt.s, L.q, kv.k, kv.v, kv_layout_of(kv), bt.pos, bf.state, bf.plan,
-                  bt.scale, bf.out, bf.logits, bf.workspace, events=timer)
+    B.decode_step(v.p, bt.s, L.q, kv.k, kv.v, kv_layout_of(kv, v.ring_rows), bt.pos, bf.state,
+                  bf.plan, bt.scale, bf.out, bf.logits, bf.workspace, events=timer)
 
 
 def step(bt: Batch, dense: bool = False, timers=None, fused: bool = False,

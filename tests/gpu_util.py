@@ -161,11 +161,7 @@ def c_replay_states(N_r, N_att, L, ts, Hkv, rng, threads=8):
 
     def one(job):
         b, h, t, rand = job
-        skip_used, kept = coracle.alg1_replay(N_r, N_att, L, t, rand)
-        st = alg1.HeadState(N_r, N_att)
-        # the list before step t's shift, and the positions evicted before t
-        st.skip_idx = [j - 1 for j in skip_used] if st.phase(t) >= 2 else list(skip_used)
-        st.evicted = set(range(0, max(0, t - N_r)))
+        st, kept = coracle.replay_head(N_r, N_att, L, t, rand)
         return b, h, st, kept
 
     states = [[None] * Hkv for _ in ts]

@@ -195,3 +195,23 @@ def test_benchmark_launch_configs(name, mode):
     li = B.launch_info(p, s)
     got = (li.rows_per_split, li.max_splits, li.workgroups, li.waves_per_group, li.kernel_variant)
     assert got == BENCH_CONFIGS[(name, mode)]
+
+
+def test_binding_rejects_bad_tensors_before_the_call():
+    """The binding checks device, element type, density and size of every
+    tensor it passes; a mismatch raises before any pointer reaches the
+    library (so this needs no GPU)."""
+    import torch
+    p = B.make_params(8, 4, 4, 8, 3)
+    s = B.make_shape(2, 4, 2, 64)
+    q = torch.zeros((2, 4, 64), dtype=torch.bfloat16)
+    k = torch.zeros((2, 2, 24, 64), dtype=torch.bfloat16)
+    out = torch.zeros((2, 4, 64), dtype=torch.float32)
+    pos = torch.zeros(2, dtype=torch.int32)
+    lay = B.kv_layout(k)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.decode_attention(p, s, q, k, k, lay, pos, None, 0.1, out)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.decode_step(p, s, q, k, k, lay, pos, None, None, 0.1, out, None)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        B.plan(p, s, pos, None, torch.zeros(B.plan_bytes(p, s), dtype=torch.uint8))

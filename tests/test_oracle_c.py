@@ -118,3 +118,17 @@ def test_c_request_step_threads_and_empty_prompt():
         assert np.array_equal(st.skip, outs[0][1].skip)
     res = ostep.request_step(17, q, Kp, Vp, K, V, 0.2, "diagonal", copy.deepcopy(heads))
     assert np.abs(outs[0][0][0] - res.out).max() <= 1e-12 * np.abs(res.out).max()
+
+
+def test_replay_head_is_the_state_before_the_step():
+    rng = random.Random(9)
+    for N_r, N_att, L in ((7, 4, 20), (12, 3, 40), (30, 30, 70)):
+        for t in range(L):
+            rand = [rng.randrange(1 << 40) for _ in range(N_r)]
+            st, kept = coracle.replay_head(N_r, N_att, L, t, rand)
+            ref = alg1.HeadState(N_r, N_att)
+            ch = alg1.uniform(rand)
+            for u in range(t):
+                ref.step(u, ch)
+            assert st.skip_idx == ref.skip_idx and st.evicted == ref.evicted, (N_r, N_att, t)
+            assert ref.step(t, lambda t_, i_: 0).idx == kept
