@@ -114,16 +114,22 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->S = static_cast<int>(S);
   // Waves per workgroup: the most tiles any split has (tiles stop at the
   // prompt/decode boundary, so a split can have one more than C / tile).
-  int64_t max_tiles = 1;
-  for (int64_t sp = 0; sp < S; ++sp) {
-    const int64_t r0 = sp * C, r1 = std::min(rows_max, r0 + C);
-    const int64_t pe = std::min<int64_t>(r1, d->Lp);
-    const int64_t wst = std::max<int64_t>(r0, d->Lp);
-    const int64_t tiles = (pe > r0 ? (pe - r0 + block_rows - 1) / block_rows : 0) +
-                          (r1 > wst ? (r1 - wst + block_rows - 1) / block_rows : 0);
-    max_tiles = std::max(max_tiles, tiles);
-  }
-  d->NW = static_cast<int>(std::min<int64_t>(kWaves, max_tiles));
+  // fp8 caches load twice the elements per lane, so the vector-ALU tile
+  // holds twice the rows (at most 64) and a split has fewer tiles.
+  auto waves_for = [&](int64_t tile_rows) {
+    int64_t max_tiles = 1;
+    for (int64_t sp = 0; sp < S; ++sp) {
+      const int64_t r0 = sp * C, r1 = std::min(rows_max, r0 + C);
+      const int64_t pe = std::min<int64_t>(r1, d->Lp);
+      const int64_t wst = std::max<int64_t>(r0, d->Lp);
+      const int64_t tiles = (pe > r0 ? (pe - r0 + tile_rows - 1) / tile_rows : 0) +
+                            (r1 > wst ? (r1 - wst + tile_rows - 1) / tile_rows : 0);
+      max_tiles = std::max(max_tiles, tiles);
+    }
+    return static_cast<int>(std::min<int64_t>(d->MF ? kWavesMfma : kWaves, max_tiles));
+  };
+  d->NW = waves_for(block_rows);
+  d->NW_fp8 = waves_for(d->MF ? kMfmaTile : 2 * rows_per_instr * unroll_for(G, d->D, 1));
   d->ws_bytes = S > 1 ? static_cast<size_t>(pairs) * S * G * (d->D + 2) * sizeof(float) : 0;
   return DSA_OK;
 }

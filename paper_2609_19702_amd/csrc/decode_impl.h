@@ -9,15 +9,16 @@
 // ascending position (dense mode: decode rows 0 .. t).  Split s covers keys
 // [s*C, min(n, (s+1)*C)).
 //
-// Data path (HBM-bound: each bf16 K/V element is read once and used for one
+// Data path (HBM-bound: each K/V element is read once and used for one
 // multiply-add per query head of the group):
-//   - a lane loads 16 bytes (8 bf16) of a row, so a 64-lane wave loads
-//     512/d rows per instruction with 128-bit coalesced accesses (one row =
-//     d/8 consecutive lanes = one contiguous 128/256-byte segment);
-//   - a wave works on tiles of U load instructions (U*512/d rows) and issues
-//     every K and V load of a tile before using any of them; rows past the
-//     end of the split read a valid row and get weight 0, so no load sits
-//     behind a branch;
+//   - a lane loads 16 bytes of a row (8 bf16 or 16 fp8 elements), so a
+//     64-lane wave loads 512/d (bf16) or 1024/d (fp8) rows per instruction
+//     with 128-bit coalesced accesses (one row = consecutive lanes covering
+//     one contiguous 64- to 256-byte segment);
+//   - a wave works on tiles of U load instructions (at most 64 rows) and
+//     issues every K and V load of a tile before using any of them; rows
+//     past the end of the split read a valid row and get weight 0, so no
+//     load sits behind a branch;
 //   - tiles hold either prompt rows or kept decode rows, never both; the
 //     kept positions of a window tile are held one per lane and handed to
 //     the row groups with ds_bpermute, prompt tiles need none;
@@ -60,43 +61,49 @@
 namespace dsa {
 namespace {
 
-// K/V element types.  A lane always owns 8 consecutive elements of a row
-// (16 bytes of bf16, 8 bytes of fp8), so the tiling, the row groups and the
-// reductions are the same for both; only the load and the widening to fp32
-// (or to the bf16 MFMA operand) differ.
+// K/V element types.  A lane always loads 16 consecutive bytes of a row (one
+// 128-bit access): 8 bf16 elements or 16 fp8 elements (kEpl).  The tiles,
+// row groups and reductions follow from the lanes per row, D / kEpl; only
+// the widening to fp32 (or to the bf16 MFMA operand) differs.
 struct KvBf16 {
   static constexpr int kBytes = 2;
+  static constexpr int kEpl = 8;
   using Raw = uint4;
   static __device__ __forceinline__ Raw load(const uint8_t* p) { return load_stream16(p); }
   static __device__ __forceinline__ void widen(const Raw& r, float (&f)[8]) { unpack8(r, f); }
-  static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r) {
+  // The bf16 MFMA operand of elements 8*half .. 8*half + 7 of a load.
+  static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r, int /*half*/) {
     return __builtin_bit_cast(bf16x8, r);
   }
 };
 
 struct KvFp8 {
   static constexpr int kBytes = 1;
-  using Raw = uint2;
-  static __device__ __forceinline__ Raw load(const uint8_t* p) { return load_stream8(p); }
+  static constexpr int kEpl = 16;
+  using Raw = uint4;
+  static __device__ __forceinline__ Raw load(const uint8_t* p) { return load_stream16(p); }
   // v_cvt_pk_f32_fp8 widens two OCP E4M3 bytes (the low or the high half of
   // a word) to fp32 exactly.
-  static __device__ __forceinline__ void widen(const Raw& r, float (&f)[8]) {
-    const uint32_t w[2] = {r.x, r.y};
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), false);
-      const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w[i]), true);
-      f[4 * i + 0] = lo[0];
-      f[4 * i + 1] = lo[1];
-      f[4 * i + 2] = hi[0];
-      f[4 * i + 3] = hi[1];
-    }
+  static __device__ __forceinline__ void widen_word(uint32_t w, float* f) {
+    const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), false);
+    const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), true);
+    f[0] = lo[0];
+    f[1] = lo[1];
+    f[2] = hi[0];
+    f[3] = hi[1];
+  }
+  static __device__ __forceinline__ void widen(const Raw& r, float (&f)[16]) {
+    widen_word(r.x, f);
+    widen_word(r.y, f + 4);
+    widen_word(r.z, f + 8);
+    widen_word(r.w, f + 12);
   }
   // Every E4M3 value is a bf16 value (4 significant bits, exponents
   // -9 .. 8), so keeping the high half of the fp32 bits is exact.
-  static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r) {
+  static __device__ __forceinline__ bf16x8 to_bf16(const Raw& r, int half) {
     float f[8];
-    widen(r, f);
+    widen_word(half ? r.z : r.x, f);
+    widen_word(half ? r.w : r.y, f + 4);
     uint32_t w[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -281,8 +288,8 @@ __device__ int count_kept(const SkipSet& ss, int lane) {
 // One butterfly step of the log-sum-exp merge of per-lane partial results
 // (running max m, sum l, weighted values acc) across lanes l and l ^ OFF.
 // Every lane whose bit OFF is clear combines (own, partner) in that order.
-template <int OFF, int G>
-__device__ __forceinline__ void merge_groups(float (&m)[G], float (&l)[G], float (&acc)[G][8]) {
+template <int OFF, int G, int EPL>
+__device__ __forceinline__ void merge_groups(float (&m)[G], float (&l)[G], float (&acc)[G][EPL]) {
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     float m1, m2, l1, l2;
@@ -293,7 +300,7 @@ __device__ __forceinline__ void merge_groups(float (&m)[G], float (&l)[G], float
     const float a2 = fast_exp2(m2 - mn);
     l[g] = fmaf(l1, a1, l2 * a2);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < EPL; ++e) {
       float x1, x2;
       xor_pair<OFF>(acc[g][e], x1, x2);
       acc[g][e] = fmaf(x1, a1, x2 * a2);
@@ -338,12 +345,17 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
                                           const uint8_t* vb, const bf16x8* qb, int b, int kvh,
                                           int w0, float sl, float sl2, float& m_c, float& l_c,
                                           f32x4 (&oacc)[D / 16], float* wls, uint16_t* vt) {
-  constexpr int LPR = D / 8, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
+  constexpr int EPL = KV::kEpl;  // elements per 16-byte load
+  constexpr int KPL = EPL / 8;    // MFMA k-steps per K load
+  constexpr int LPR = D / EPL, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
   constexpr int NH = T / 16;  // 16-row MFMA blocks per tile
   constexpr int VROW = D + kVPad;
   static_assert(NH == 2, "the P.V row order assumes two 16-row blocks");
   const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR, c = lane % LPR;
-  typename KV::Raw kr[NH][NK];
+  // K load li of lane group lq holds elements 32*KPL*li + EPL*lq .. + EPL-1,
+  // the A operands of k-steps KPL*li .. KPL*li + KPL-1 (the queries use the
+  // same element order; q.k does not depend on it).
+  typename KV::Raw kr[NH][NK / KPL];
 #pragma unroll
   for (int h = 0; h < NH; ++h) {
     const int r = rs + 16 * h + lr;
@@ -351,7 +363,8 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
     int cr = 0;  // rows past the tile end read row 0 and get weight 0
     if (r < re) cr = has_win ? a.Lp + wpos : r;
 #pragma unroll
-    for (int i = 0; i < NK; ++i) kr[h][i] = KV::load(kmf + cr * a.sr + 32 * KV::kBytes * i);
+    for (int li = 0; li < NK / KPL; ++li)
+      kr[h][li] = KV::load(kmf + cr * a.sr + 32 * KPL * KV::kBytes * li);
   }
   typename KV::Raw vr[UV];
 #pragma unroll
@@ -368,8 +381,8 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
     sc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < NK; ++i)
-      sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(KV::to_bf16(kr[h][i]), qb[i], sc[h], 0, 0,
-                                                      0);
+      sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(KV::to_bf16(kr[h][i / KPL], i % KPL), qb[i],
+                                                      sc[h], 0, 0, 0);
   }
   if (has_win && lr < G) {
 #pragma unroll
@@ -389,7 +402,10 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
   // V rows of the tile into the wave's LDS tile, as bf16 (exact for fp8).
 #pragma unroll
   for (int u = 0; u < UV; ++u)
-    *reinterpret_cast<bf16x8*>(vt + (u * RPI + rg) * VROW + c * 8) = KV::to_bf16(vr[u]);
+#pragma unroll
+    for (int hf = 0; hf < KPL; ++hf)
+      *reinterpret_cast<bf16x8*>(vt + (u * RPI + rg) * VROW + c * EPL + 8 * hf) =
+          KV::to_bf16(vr[u], hf);
   // Scores in log2 units, rounded once, so the largest one gets weight
   // exactly 1.
   float s2[NH][4];
@@ -465,19 +481,22 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
 
 template <class KV, int D, int G, int U, bool FUSED, bool MF>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
-  constexpr int LPR = D / 8;       // lanes per row (V layout; K layout too without MF)
+  constexpr int EPL = KV::kEpl;    // elements a lane loads per 16-byte access
+  constexpr int LPR = D / EPL;     // lanes per row (V layout; K layout too without MF)
   constexpr int RPI = 64 / LPR;    // rows per load instruction
-  constexpr int T = MF ? kMfmaTile : RPI * U;  // rows per wave tile (<= 64)
-  constexpr int UV = T / RPI;      // V load instructions per tile
+  constexpr int UU = MF ? U : unroll_for(G, D, KV::kBytes);  // loads in flight per operand
+  constexpr int T = MF ? kMfmaTile : RPI * UU;      // rows per wave tile (<= 64)
   constexpr int NK = D / 32;       // MFMA k-steps per 16 rows (MF only)
+  constexpr int KPL = EPL / 8;     // MFMA k-steps per K load (MF only)
   static_assert(T <= 64, "one kept position per lane");
   static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
   constexpr int KS = FUSED ? max_fused_split(MF) : 1;
   // The per-wave partial results (red) and, in the MFMA tile, the per-wave
   // V tiles share one LDS block: the V tiles are dead once every wave has
   // left the tile loop.
-  constexpr int kRedBytes = kWaves * G * (D + 2) * 4;
-  constexpr int kVtBytes = MF ? kWaves * kMfmaTile * (D + kVPad) * 2 : 0;
+  constexpr int NWMAX = MF ? kWavesMfma : kWaves;  // waves of a workgroup at most
+  constexpr int kRedBytes = NWMAX * G * (D + 2) * 4;
+  constexpr int kVtBytes = MF ? NWMAX * kMfmaTile * (D + kVPad) * 2 : 0;
   __shared__ __attribute__((aligned(16)))
   unsigned char smem[kRedBytes > kVtBytes ? kRedBytes : kVtBytes];
   float (*red)[G][D + 2] = reinterpret_cast<float (*)[G][D + 2]>(smem);
@@ -491,7 +510,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   const int rg = lane / LPR;       // row group within the wave
-  const int c = lane % LPR;        // 8-element column chunk
+  const int c = lane % LPR;        // EPL-element column chunk
   const int s = blockIdx.x % a.S;
   const int pair = blockIdx.x / a.S;
   const int kvh = pair % a.Hkv;
@@ -506,12 +525,14 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   // decode position either: a wave that may own window rows loads them now
   // too, so the kept set is ready one memory latency sooner.
   // Queries first: their address depends on nothing loaded.
-  uint4 qr[MF ? 1 : G];
+  uint4 qr[MF ? 1 : G][EPL / 8];
   if constexpr (!MF) {
 #pragma unroll
     for (int g = 0; g < G; ++g)
-      qr[g] = *reinterpret_cast<const uint4*>(
-          a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + (lane % LPR) * 8);
+#pragma unroll
+      for (int hf = 0; hf < EPL / 8; ++hf)
+        qr[g][hf] = *reinterpret_cast<const uint4*>(
+            a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * D + (lane % LPR) * EPL + 8 * hf);
   }
   const int r0 = s * a.C;
   const int32_t* dummy32 = reinterpret_cast<const int32_t*>(a.q);
@@ -552,7 +573,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   // Byte offset of this lane's first element (strides arrive in bytes).
   constexpr int E = KV::kBytes;
   const int64_t base = (a.row_base ? rb_raw * E : static_cast<int64_t>(b) * a.sb) +
-                       static_cast<int64_t>(kvh) * a.sh + c * 8 * E;
+                       static_cast<int64_t>(kvh) * a.sh + c * EPL * E;
   const uint8_t* kb = a.k + base;
   const uint8_t* vb = a.v + base;
   // fp8 caches: the K scale folds into the logit scale, the V scale into
@@ -561,11 +582,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const float sl2 = kScaled && a.ks ? a.scale_log2 * ks_raw : a.scale_log2;
   const int32_t* widx = FUSED ? nullptr : a.idx + static_cast<size_t>(pair) * a.plan_cap - a.Lp;
 
-  // MFMA operands: K in the A layout (lane l: row l%16, elements
-  // 8*(l/16) + 32*i .. +7 of k-step i), q^T in the B layout (lane l: query
-  // head l%16 of the group, same elements; zero for l%16 >= G).
+  // MFMA operands: K in the A layout (lane l: row l%16; k-step i takes the
+  // 8 elements 32*KPL*(i/KPL) + EPL*(l/16) + 8*(i%KPL) .. +7, so one 16-byte
+  // load serves KPL k-steps), q^T in the B layout (lane l: query head l%16
+  // of the group, the same elements; zero for l%16 >= G).
   const int lr = lane & 15, lq = lane >> 4;
-  const uint8_t* kmf = a.k + (base - c * 8 * E) + 8 * E * lq;
+  const uint8_t* kmf = a.k + (base - c * EPL * E) + EPL * E * lq;
   bf16x8 qb[MF ? NK : 1];
   if constexpr (MF) {
 #pragma unroll
@@ -573,7 +595,8 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       uint4 x = make_uint4(0, 0, 0, 0);
       if (lr < G)
         x = *reinterpret_cast<const uint4*>(
-            a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + lr) * D + 32 * i + 8 * lq);
+            a.q + (static_cast<size_t>(b) * a.Hq + kvh * G + lr) * D +
+            32 * KPL * (i / KPL) + EPL * lq + 8 * (i % KPL));
       qb[i] = __builtin_bit_cast(bf16x8, x);
     }
   }
@@ -605,14 +628,14 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   // K loads before the ranking below, so they are in flight while the window
   // rows are ranked (V too would not fit in 128 registers).
   constexpr bool kHoist = FUSED && !MF;
-  typename KV::Raw kr[U], vr[U];  // the vector-ALU tile's K/V
+  typename KV::Raw kr[UU], vr[UU];  // the vector-ALU tile's K/V
   const bool pre = kHoist && wave < P;
   if constexpr (kHoist) {
     if (pre) {
       const int rs = r0 + wave * T;
       const int re = min(rs + T, pe);
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
+      for (int u = 0; u < UU; ++u) {
         const int r = rs + u * RPI + rg;
         const int cr = r < re ? r : 0;  // rows past the tile end read row 0, weight 0
         kr[u] = KV::load(kb + cr * a.sr);
@@ -657,15 +680,23 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     }
   }
 
-  float qf[MF ? 1 : G][8];
-  float m[G], l[G], acc[G][8];
+  float qf[MF ? 1 : G][EPL];
+  float m[G], l[G], acc[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    if constexpr (!MF) unpack8(qr[g], qf[g]);
+    if constexpr (!MF) {
+#pragma unroll
+      for (int hf = 0; hf < EPL / 8; ++hf) {
+        float f8[8];
+        unpack8(qr[g][hf], f8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) qf[g][8 * hf + e] = f8[e];
+      }
+    }
     m[g] = kNegBig;
     l[g] = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[g][e] = 0.f;
+    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
   }
   float m_c = kNegBig, l_c = 0.f;  // MF: running max / partial sum of head lr
   f32x4 oacc[MF ? D / 16 : 1];     // MF: output, C layout (heads x 16 columns per block)
@@ -690,13 +721,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       if (a.ring && pos_l >= a.Ns) pos_l = a.Ns + (pos_l - a.Ns) % a.ring;  // ring slot
     }
     if constexpr (MF) {
-      if constexpr (MF)
-        mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
-                                   sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
+      mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
+                                 sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
       return;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < UU; ++u) {
       const int r = rs + u * RPI + rg;
       const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
       int cr = 0;  // rows past the tile end read row 0 and get weight 0
@@ -707,22 +737,22 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     // Every load of the tile is issued before any arithmetic on it.
     __builtin_amdgcn_sched_barrier(0);
 
-    float sc[U][G];
+    float sc[UU][G];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float kf[8];
+    for (int u = 0; u < UU; ++u) {
+      float kf[EPL];
       KV::widen(kr[u], kf);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float x = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x = fmaf(qf[g][e], kf[e], x);
+        for (int e = 0; e < EPL; ++e) x = fmaf(qf[g][e], kf[e], x);
         sc[u][g] = group_sum<LPR>(x);
       }
     }
     if (has_win && c == 0) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
+      for (int u = 0; u < UU; ++u) {
         const int r = rs + u * RPI + rg;
         if (r < re) {
 #pragma unroll
@@ -742,7 +772,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       // exactly 1.
       float mx = kNegBig;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
+      for (int u = 0; u < UU; ++u) {
         sc[u][g] = rs + u * RPI + rg < re ? sc[u][g] * sl2 : kNegBig;
         mx = fmaxf(mx, sc[u][g]);
       }
@@ -751,11 +781,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       m[g] = mnew;
       l[g] *= alpha;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[g][e] *= alpha;
+      for (int e = 0; e < EPL; ++e) acc[g][e] *= alpha;
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float vf[8];
+    for (int u = 0; u < UU; ++u) {
+      float vf[EPL];
       KV::widen(vr[u], vf);
       const bool ok = rs + u * RPI + rg < re;
 #pragma unroll
@@ -763,7 +793,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
         const float p = ok ? fast_exp2(sc[u][g] - m[g]) : 0.f;
         l[g] += p;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
       }
     }
   };
@@ -814,15 +844,16 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
   // Merge the row groups of the wave (lanes c, c + LPR, c + 2*LPR, ...).
   if constexpr (!MF) {
-    if constexpr (LPR == 8) merge_groups<8, G>(m, l, acc);
-    merge_groups<16, G>(m, l, acc);
-    merge_groups<32, G>(m, l, acc);
+    if constexpr (LPR <= 4) merge_groups<4, G, EPL>(m, l, acc);
+    if constexpr (LPR <= 8) merge_groups<8, G, EPL>(m, l, acc);
+    merge_groups<16, G, EPL>(m, l, acc);
+    merge_groups<32, G, EPL>(m, l, acc);
   }
   if (!MF && rg == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) red[wave][g][c * 8 + e] = acc[g][e];
+      for (int e = 0; e < EPL; ++e) red[wave][g][c * EPL + e] = acc[g][e];
       if (c == 0) {
         red[wave][g][D] = m[g];
         red[wave][g][D + 1] = l[g];
@@ -903,7 +934,7 @@ void decode_kernel(DecodeArgs a) {
 // blocks in registers; the occupancy floor keeps three waves per SIMD
 // resident.
 template <class KV, int D, int G, bool FUSED>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3, 8)))
+__global__ __launch_bounds__(64 * kWavesMfma) __attribute__((amdgpu_waves_per_eu(3, 8)))
 void decode_mfma_kernel(DecodeArgs a) {
   decode_body<KV, D, G, 2, FUSED, true>(a);
 }
@@ -1016,8 +1047,9 @@ template <class KV, int D, int G, int U, bool FUSED, bool MF>
 void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                   hipEvent_t t1) {
   const int grid = d.B * d.Hkv * d.S;
-  const int block = 64 * d.NW;
-  const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * d.NW * a.words) : 0u;
+  const int nw = KV::kBytes == 1 ? d.NW_fp8 : d.NW;
+  const int block = 64 * nw;
+  const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u;
   if constexpr (MF) {
     if (t0 || t1)
       hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED>, dim3(grid), dim3(block), lds, st,

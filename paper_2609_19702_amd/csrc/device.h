@@ -33,13 +33,6 @@ __device__ __forceinline__ uint4 load_stream16(const void* p) {
   return make_uint4(x.x, x.y, x.z, x.w);
 }
 
-// 8-byte form of the same (8 fp8 elements of a row).
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint2 load_stream8(const void* p) {
-  const u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
-  return make_uint2(x.x, x.y);
-}
-
 // DPP lane permutations inside a 16-lane row.
 constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm [1,0,3,2]: lane ^ 1
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm [2,3,0,1]: lane ^ 2
@@ -53,29 +46,38 @@ __device__ __forceinline__ float dpp(float x) {
       float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of N lanes (N = 8 or 16); every lane of a group
-// receives the group's sum.  Pure DPP: no LDS traffic.
+// Sum over aligned groups of N lanes (N = 4, 8 or 16); every lane of a
+// group receives the group's sum.  Pure DPP: no LDS traffic.
 template <int N>
 __device__ __forceinline__ float group_sum(float x) {
-  static_assert(N == 8 || N == 16, "group of 8 or 16 lanes");
+  static_assert(N == 4 || N == 8 || N == 16, "group of 4, 8 or 16 lanes");
   x += dpp<kDppQuadSwap1>(x);
   x += dpp<kDppQuadSwap2>(x);
-  x += dpp<kDppHalfMirror>(x);
+  if constexpr (N >= 8) x += dpp<kDppHalfMirror>(x);
   if constexpr (N == 16) x += dpp<kDppRowMirror>(x);
   return x;
 }
 
+// ds_swizzle in bit mode: lane i reads lane i ^ 4 within each 32-lane half
+// (and mask 0x1f, or mask 0, xor mask 4).
+constexpr int kSwizzleXor4 = 0x1F | (4 << 10);
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// One step of a butterfly across lanes l and l ^ OFF (OFF = 8, 16 or 32)
-// without the LDS crossbar: a DPP row rotate for 8, the gfx950 lane swaps
-// (v_permlane16_swap / v_permlane32_swap) for 16 and 32.  Gives the pair as
-// (first, second) with first the value of the lane whose bit OFF is clear,
-// so every lane of that half sees (own, partner).
+// One step of a butterfly across lanes l and l ^ OFF (OFF = 4, 8, 16 or 32)
+// without a trip through LDS memory: ds_swizzle for 4, a DPP row rotate for
+// 8, the gfx950 lane swaps (v_permlane16_swap / v_permlane32_swap) for 16
+// and 32.  Gives the pair as (first, second) with first the value of the
+// lane whose bit OFF is clear, so every lane of that half sees (own,
+// partner).
 template <int OFF>
 __device__ __forceinline__ void xor_pair(float x, float& first, float& second) {
-  static_assert(OFF == 8 || OFF == 16 || OFF == 32, "butterfly step of 8, 16 or 32 lanes");
-  if constexpr (OFF == 8) {
+  static_assert(OFF == 4 || OFF == 8 || OFF == 16 || OFF == 32,
+                "butterfly step of 4, 8, 16 or 32 lanes");
+  if constexpr (OFF == 4) {
+    first = x;
+    second = __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(x), kSwizzleXor4));
+  } else if constexpr (OFF == 8) {
     first = x;
     second = dpp<kDppRowRor8>(x);
   } else {

@@ -26,7 +26,8 @@ struct Derived {
   int U;          // loads in flight per wave per operand (unroll_of(G))
   int C;          // rows per split workgroup
   int S;          // splits per (request, KV head), upper bound
-  int NW;         // waves per decode workgroup (1..kWaves)
+  int NW;         // waves per decode workgroup (1..kWaves), bf16 caches
+  int NW_fp8;     // the same for fp8 caches (tiles of twice the rows)
   bool MF;        // grouped query heads on the MFMA tile (uses_mfma_tile(G))
   size_t ws_bytes;
 };
@@ -64,12 +65,21 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #ifndef DSA_TUNE_UNROLL
 #define DSA_TUNE_UNROLL 0  // loads in flight per wave (2, 4 or 8); 0: by group size
 #endif
+#ifndef DSA_TUNE_UNROLL_FP8
+#define DSA_TUNE_UNROLL_FP8 6  // loads in flight per wave and operand on fp8 caches, at most
+#endif                         // (8 spills registers at d = 128: 73 us against 59 us per
+                               // Janus-like layer; 4 gives 61 us)
+#ifndef DSA_TUNE_MFMA_WAVES
+#define DSA_TUNE_MFMA_WAVES 4  // most waves per workgroup of the grouped-head MFMA tile
+#endif
 #ifndef DSA_TUNE_VALU_GQA
 #define DSA_TUNE_VALU_GQA 0  // 1: grouped query heads on the vector-ALU tile instead of MFMA
 #endif
 
-constexpr int kWaves = 4;          // waves per workgroup in every kernel
+constexpr int kWaves = 4;          // waves per workgroup (the MFMA decode tile: kWavesMfma)
 constexpr int kBlock = 64 * kWaves;
+constexpr int kWavesMfma = DSA_TUNE_MFMA_WAVES;
+static_assert(kWavesMfma >= 1 && kWavesMfma <= 16, "MFMA workgroup waves");
 constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
 constexpr int kMaxFusedSplit = DSA_TUNE_MAX_FUSED_SPLIT;
 constexpr int kMaxFusedSplitMfma = DSA_TUNE_MAX_FUSED_SPLIT_MFMA;
@@ -91,6 +101,17 @@ constexpr int unroll_of(int G) {
   return (DSA_TUNE_UNROLL == 2 || DSA_TUNE_UNROLL == 4 || DSA_TUNE_UNROLL == 8)
              ? DSA_TUNE_UNROLL
              : (G >= 8 ? 2 : (G >= 4 ? 4 : 8));
+}
+// The same for a cache of `elem_bytes`-byte elements and head_dim d: a tile
+// holds at most 64 rows (one kept position per lane), and fp8 caches may be
+// capped lower.  A lane loads 16 bytes, so one instruction covers
+// 1024 / (d * elem_bytes) rows.
+constexpr int unroll_for(int G, int d, int elem_bytes) {
+  const int rpi = 1024 / (d * elem_bytes);
+  int u = unroll_of(G);
+  if (rpi * u > 64) u = 64 / rpi;
+  if (elem_bytes == 1 && u > DSA_TUNE_UNROLL_FP8) u = DSA_TUNE_UNROLL_FP8;
+  return u;
 }
 constexpr int kMaxFusedWindow = 16384;  // N_r of the fused step (skip bitmap per wave in LDS)
 constexpr float kNegBig = -1.0e30f;  // "no score yet": finite, so exp2 of a difference is 0

@@ -2,13 +2,14 @@
 
 * every finite E4M3 byte widens exactly, read back through the window logits
   (one-hot queries, unit scales) on the vector-ALU and the MFMA tiles;
-* with unit scales an fp8 cache gives bit for bit the outputs of the bf16
-  cache holding the same values (the two share every instruction but the
-  load), in both modes and both tiles;
+* with unit scales an fp8 cache gives the kept sets of the bf16 cache
+  holding the same values, and its outputs and window logits within fp32
+  rounding (an fp8 lane loads 16 elements, a bf16 lane 8, so the sums run
+  in different orders), in both modes and both tiles;
 * scaled caches from the synthetic quantizer match the oracle, which decodes
   the bytes exactly and multiplies by the scales in fp64, within the
   tolerance; the fused step reproduces the separate calls bit for bit, a
-  ring reproduces the linear cache bit for bit;
+  ring reproduces the linear cache bit for bit and matches the oracle;
 * argument errors: scales on a bf16 cache, unknown element types."""
 
 import copy
@@ -23,7 +24,8 @@ from oracle import fp8 as ofp8
 from oracle import step as ostep
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import DEV, TOL, check_layer_vs_oracle, dot_band, rel_err, say, states_to_buffer
+from tests.gpu_util import (DEV, TOL, check_layer_vs_oracle, dot_band, offsets_from_buffer, rel_err,
+                            say, states_to_buffer, within_tie_band)
 
 pytestmark = pytest.mark.gpu
 
@@ -136,10 +138,14 @@ def test_fp8_matches_oracle(case, mode):
 
 @pytest.mark.parametrize("mode", [B.MODE_DIAGONAL, B.MODE_DENSE])
 @pytest.mark.parametrize("case", CASES[:4], ids=[str(c) for c in CASES[:4]])
-def test_unit_scale_fp8_equals_bf16_bitwise(case, mode):
-    """Bytes with unit scales and the bf16 cache of their values run the same
-    arithmetic in the same order."""
-    say("fp8 = bf16", case, mode)
+def test_unit_scale_fp8_matches_bf16(case, mode):
+    """Bytes with unit scales (given, or absent) and the bf16 cache of their
+    values: the same kept sets and, within fp32 rounding, the same outputs
+    and window logits.  (Not bit for bit: an fp8 lane loads 16 elements, a
+    bf16 lane 8, so the two sum in different orders.)  A unit scale and no
+    scale give identical bits.  Each selection either agrees or both picks
+    lie inside the certified tie band."""
+    say("fp8 ~ bf16", case, mode)
     w, kv, q, ts, p, s, states = make_case(case, mode, seed=4)
     kb = kv.k.view(torch.float8_e4m3fn).to(torch.bfloat16)
     vb = kv.v.view(torch.float8_e4m3fn).to(torch.bfloat16)
@@ -158,12 +164,38 @@ def test_unit_scale_fp8_equals_bf16_bitwise(case, mode):
         else:
             B.decode_attention(p, s, q, k, v, lay, pos, None, 0.125, bufs.out, None, bufs.workspace)
         torch.cuda.synchronize()
-        outs.append((bufs.out.clone(), st.clone(), bufs.logits.clone()))
-    for o in outs[1:]:
-        assert torch.equal(o[0], outs[0][0])
-        assert torch.equal(o[1], outs[0][1])
-        if sparse:
-            assert torch.equal(o[2], outs[0][2])
+        outs.append((bufs.out.clone(), st.clone(), bufs.logits.clone(), bufs.plan.clone()))
+    assert all(torch.equal(x, y) for x, y in zip(outs[1], outs[2]))
+    (o0, s0, l0, p0), (o1, s1, l1, p1) = outs[0], outs[1]
+    d = (o1 - o0).abs().amax(dim=-1) / o0.abs().amax(dim=-1).clamp_min(1e-30)
+    assert d.max().item() <= 1e-5, d.max().item()
+    if not sparse:
+        return
+    assert torch.equal(p0, p1)
+    assert (l1 - l0).abs().max().item() <= 1e-5 * max(1.0, l0.abs().max().item())
+    if torch.equal(s0, s1):
+        return
+    # a selection that differs: both picks must be near ties of the exact scores
+    Hkv, g = s.num_kv_heads, s.num_q_heads // s.num_kv_heads
+    cnt, _, idx = (x.cpu().numpy() for x in B.plan_views(p, s, p0))
+    _, _, off0 = offsets_from_buffer(p, s, s0)
+    c1, _, off1 = offsets_from_buffer(p, s, s1)
+    qn = q.double().cpu().numpy()
+    for b, t in enumerate(ts):
+        Kp, Vp, K, V = fp8_request_arrays(kv, b, w.prompt_len, Hkv)
+        k_slot = t - (p.n_att - 1)
+        for h in range(Hkv):
+            pair = b * Hkv + h
+            if not (0 <= k_slot < off0.shape[1]) or off0[pair, k_slot] == off1[pair, k_slot]:
+                continue
+            kept = idx[pair, :cnt[pair]].tolist()
+            j0 = kept.index(t - int(off0[pair, k_slot]))
+            j1 = kept.index(t - int(off1[pair, k_slot]))
+            qg = qn[b][h * g:(h + 1) * g]
+            from oracle.attention import select
+            j_ref, _ = select(qg, K[h][kept], 0.125)
+            assert within_tie_band(qg, K[h][kept], 0.125, j0, j_ref)
+            assert within_tie_band(qg, K[h][kept], 0.125, j1, j_ref)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(c) for c in CASES])
