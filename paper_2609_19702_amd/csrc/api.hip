@@ -101,8 +101,9 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   int64_t c_target = std::max<int64_t>(block_rows, split_bytes / (4 * d->D));
   if (sparse) c_target = std::min<int64_t>(c_target, max_fused_split(d->MF));
   int64_t S = std::max<int64_t>(1, (rows_max + c_target - 1) / c_target);
-  if (pairs * S < kMinWorkgroups) {
-    const int64_t want = (kMinWorkgroups + pairs - 1) / pairs;
+  const int64_t min_wgs = sparse ? kMinWorkgroupsSparse : kMinWorkgroups;
+  if (pairs * S < min_wgs) {
+    const int64_t want = (min_wgs + pairs - 1) / pairs;
     const int64_t most = std::max<int64_t>(1, (rows_max + block_rows - 1) / block_rows);
     S = std::max<int64_t>(S, std::min(want, most));
   }
@@ -126,7 +127,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
                             (r1 > wst ? (r1 - wst + tile_rows - 1) / tile_rows : 0);
       max_tiles = std::max(max_tiles, tiles);
     }
-    return static_cast<int>(std::min<int64_t>(d->MF ? kWavesMfma : kWaves, max_tiles));
+    return static_cast<int>(std::min<int64_t>(d->MF ? kWavesMfma : kWavesValu, max_tiles));
   };
   d->NW = waves_for(block_rows);
   d->NW_fp8 = waves_for(d->MF ? kMfmaTile : 2 * rows_per_instr * unroll_for(G, d->D, 1));

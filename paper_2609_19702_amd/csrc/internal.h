@@ -53,8 +53,11 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_SPLIT_KB_DENSE_MFMA 256  // dense mode, grouped query heads
 #endif
 #ifndef DSA_TUNE_MIN_WGS
-#define DSA_TUNE_MIN_WGS 512  // split further while a launch has fewer workgroups
+#define DSA_TUNE_MIN_WGS 512  // split further while a launch has fewer workgroups (dense mode)
 #endif
+#ifndef DSA_TUNE_MIN_WGS_SPARSE
+#define DSA_TUNE_MIN_WGS_SPARSE 256  // the same in the sparse modes (fewer, larger splits of
+#endif                               // single requests: 0.3-1 us per layer less at batch 1)
 #ifndef DSA_TUNE_MAX_FUSED_SPLIT
 #define DSA_TUNE_MAX_FUSED_SPLIT 512  // most rows of a sparse-mode split (the fused step keeps
                                       // their logits and positions in LDS), vector-ALU tile
@@ -69,6 +72,9 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_UNROLL_FP8 6  // loads in flight per wave and operand on fp8 caches, at most
 #endif                         // (8 spills registers at d = 128: 73 us against 59 us per
                                // Janus-like layer; 4 gives 61 us)
+#ifndef DSA_TUNE_VALU_WAVES
+#define DSA_TUNE_VALU_WAVES 4  // most waves per workgroup of the vector-ALU decode tile
+#endif
 #ifndef DSA_TUNE_MFMA_WAVES
 #define DSA_TUNE_MFMA_WAVES 4  // most waves per workgroup of the grouped-head MFMA tile
 #endif
@@ -79,6 +85,8 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 constexpr int kWaves = 4;          // waves per workgroup (the MFMA decode tile: kWavesMfma)
 constexpr int kBlock = 64 * kWaves;
 constexpr int kWavesMfma = DSA_TUNE_MFMA_WAVES;
+constexpr int kWavesValu = DSA_TUNE_VALU_WAVES;
+static_assert(kWavesValu >= 1 && kWavesValu <= kWaves, "vector-ALU workgroup waves");
 static_assert(kWavesMfma >= 1 && kWavesMfma <= 16, "MFMA workgroup waves");
 constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
 constexpr int kMaxFusedSplit = DSA_TUNE_MAX_FUSED_SPLIT;
@@ -89,6 +97,7 @@ constexpr int kSplitKbDense64 = DSA_TUNE_SPLIT_KB_DENSE_64;
 constexpr int kSplitKbDense128 = DSA_TUNE_SPLIT_KB_DENSE_128;
 constexpr int kSplitKbDenseMfma = DSA_TUNE_SPLIT_KB_DENSE_MFMA;
 constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
+constexpr int kMinWorkgroupsSparse = DSA_TUNE_MIN_WGS_SPARSE;
 static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
 static_assert(kMaxFusedSplitMfma % 64 == 0 && kMaxFusedSplitMfma <= 1024, "fused split rows");
 // Rows of one sparse-mode split at most, by tile.
