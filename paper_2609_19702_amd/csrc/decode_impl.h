@@ -601,6 +601,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     }
   }
 
+  // Ring layouts: the start of the lap that holds position t (in positions
+  // after the sinks), for the slot arithmetic of the window tiles.
+  const int ring_lap = (a.ring && rr.t >= a.Ns) ? (rr.t - a.Ns) / a.ring * a.ring : 0;
+
   // Tiles never straddle the prompt/decode boundary: the split's prompt rows
   // [r0, pe) and decode rows [wst, r1) are each cut into tiles of T rows,
   // tile j going to wave j % nwaves.  Prompt tiles and dense-mode decode
@@ -718,7 +722,14 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       } else {
         if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
       }
-      if (a.ring && pos_l >= a.Ns) pos_l = a.Ns + (pos_l - a.Ns) % a.ring;  // ring slot
+      if (a.ring && pos_l >= a.Ns) {  // ring slot: (pos - S) mod ring, after the S sinks
+        // kept positions lie in (t - ring, t], so one conditional add
+        // reduces them from the lap of t (a position outside that range
+        // only comes from a corrupt plan: it reads slot 0)
+        int sl = pos_l - a.Ns - ring_lap;
+        if (sl < 0) sl += a.ring;
+        pos_l = a.Ns + max(sl, 0);
+      }
     }
     if constexpr (MF) {
       mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
