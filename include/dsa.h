@@ -207,7 +207,7 @@ typedef struct dsa_launch_info {
   int32_t workgroups;      /* B * Hkv * S                                   */
   int32_t kernel_variant;  /* K/V loads in flight per wave (2, 4 or 8), or 100 for
                               the MFMA tile of grouped query heads (32 rows) */
-  int32_t waves_per_group; /* waves per split workgroup (1..4)              */
+  int32_t waves_per_group; /* waves per split workgroup (1..4; MFMA tile 1..8) */
   size_t workspace_bytes;  /* fp32 partials for the combine                 */
 } dsa_launch_info;
 

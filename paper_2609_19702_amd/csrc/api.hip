@@ -87,13 +87,16 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   const int64_t rows_max = d->Lp + (sparse ? d->plan_cap : ldec);
   d->rows_max = static_cast<int>(rows_max);
   // Measured on MI355X: dense splits of ~24 KB for d = 64 (long ragged rows
-  // balance better), ~96 KB for d = 128 and ~256 KB for the grouped-head
-  // tile (fewer partials to merge).  Sparse-mode splits of ~192 KB on the
-  // vector-ALU tile, so a Janus-like request (256 prompt rows and 29 kept
-  // ones) is one split: no partials, no combine kernel, and the selection
-  // stays in the decode kernel (8% faster per layer than two splits, and
-  // faster on nearly every cell of the Janus-shaped sweep with 16 or more
-  // requests); ~96 KB on the MFMA tile.  The fused step caps a split at
+  // balance better), ~96 KB for d = 128 and ~128 KB for the grouped-head
+  // tile (on two waves, several workgroups per CU).  Sparse-mode splits of
+  // ~192 KB on the vector-ALU tile, so a Janus-like request (256 prompt
+  // rows and 29 kept ones) is one split: no partials, no combine kernel,
+  // and the selection stays in the decode kernel (8% faster per layer than
+  // two splits, and faster on nearly every cell of the Janus-shaped sweep
+  // with 16 or more requests).  ~256 KB on the MFMA tile, whose eight waves
+  // keep two tiles each in flight: an Emu3-like request (256 prompt rows
+  // and 205 kept ones) is one split too (16.0 us per layer against 24.1 us
+  // with three splits and a combine).  The fused step caps a split at
   // max_fused_split rows.
   const int dense_kb = d->MF ? kSplitKbDenseMfma : (d->D == 64 ? kSplitKbDense64 : kSplitKbDense128);
   const int sparse_kb = d->MF ? kSplitKbSparseMfma : kSplitKbSparse;
@@ -127,7 +130,8 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
                             (r1 > wst ? (r1 - wst + tile_rows - 1) / tile_rows : 0);
       max_tiles = std::max(max_tiles, tiles);
     }
-    return static_cast<int>(std::min<int64_t>(d->MF ? kWavesMfma : kWavesValu, max_tiles));
+    const int cap = d->MF ? (sparse ? kWavesMfma : kWavesMfmaDense) : kWavesValu;
+    return static_cast<int>(std::min<int64_t>(cap, max_tiles));
   };
   d->NW = waves_for(block_rows);
   d->NW_fp8 = waves_for(d->MF ? kMfmaTile : 2 * rows_per_instr * unroll_for(G, d->D, 1));

@@ -322,6 +322,47 @@ constexpr int kVPad = 16;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
+// K and V of one 32-row tile of the grouped-head path, as loaded (the loads
+// of two tiles can be in flight at once: mf_load issues, mf_compute waits).
+template <class KV, int D>
+struct MfRaw {
+  static constexpr int EPL = KV::kEpl, KPL = EPL / 8, LPR = D / EPL, RPI = 64 / LPR;
+  static constexpr int NK = D / 32, UV = kMfmaTile / RPI, NH = kMfmaTile / 16;
+  typename KV::Raw k[NH][NK / KPL];
+  typename KV::Raw v[UV];
+};
+
+// Rows [rs, re) of a tile; window tiles read row Lp + pos_l of lane i for
+// row rs + i (pos_l: the kept position, or its ring slot).
+template <class KV, int D>
+__device__ __forceinline__ void mf_load(const DecodeArgs& a, int lane, int rs, int re,
+                                        bool has_win, int pos_l, const uint8_t* kmf,
+                                        const uint8_t* vb, MfRaw<KV, D>& raw) {
+  using R = MfRaw<KV, D>;
+  const int lr = lane & 15, rg = lane / R::LPR;
+  // K load li of lane group lq holds elements 32*KPL*li + EPL*lq .. + EPL-1,
+  // the A operands of k-steps KPL*li .. KPL*li + KPL-1 (the queries use the
+  // same element order; q.k does not depend on it).
+#pragma unroll
+  for (int h = 0; h < R::NH; ++h) {
+    const int r = rs + 16 * h + lr;
+    const int wpos = has_win ? __shfl(pos_l, 16 * h + lr, 64) : 0;
+    int cr = 0;  // rows past the tile end read row 0 and get weight 0
+    if (r < re) cr = has_win ? a.Lp + wpos : r;
+#pragma unroll
+    for (int li = 0; li < R::NK / R::KPL; ++li)
+      raw.k[h][li] = KV::load(kmf + cr * a.sr + 32 * R::KPL * KV::kBytes * li);
+  }
+#pragma unroll
+  for (int u = 0; u < R::UV; ++u) {
+    const int r = rs + u * R::RPI + rg;
+    const int wpos = has_win ? __shfl(pos_l, u * R::RPI + rg, 64) : 0;
+    int cr = 0;
+    if (r < re) cr = has_win ? a.Lp + wpos : r;
+    raw.v[u] = KV::load(vb + cr * a.sr);
+  }
+}
+
 // One 32-row tile of the grouped-head path, both products on the matrix
 // cores (v_mfma_f32_16x16x32_bf16).
 //
@@ -340,11 +381,11 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 // the block).  Each weight is split into two bf16 terms (hi + lo, relative
 // error about 2^-17) so the product keeps fp32-level accuracy.
 template <class KV, int D, int G, bool FUSED>
-__device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs, int re,
-                                          bool has_win, int pos_l, const uint8_t* kmf,
-                                          const uint8_t* vb, const bf16x8* qb, int b, int kvh,
-                                          int w0, float sl, float sl2, float& m_c, float& l_c,
-                                          f32x4 (&oacc)[D / 16], float* wls, uint16_t* vt) {
+__device__ __forceinline__ void mf_compute(const DecodeArgs& a, int lane, int rs, int re,
+                                           bool has_win, const MfRaw<KV, D>& raw,
+                                           const bf16x8* qb, int b, int kvh, int w0, float sl,
+                                           float sl2, float& m_c, float& l_c,
+                                           f32x4 (&oacc)[D / 16], float* wls, uint16_t* vt) {
   constexpr int EPL = KV::kEpl;  // elements per 16-byte load
   constexpr int KPL = EPL / 8;    // MFMA k-steps per K load
   constexpr int LPR = D / EPL, RPI = 64 / LPR, T = kMfmaTile, UV = T / RPI, NK = D / 32;
@@ -352,29 +393,8 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
   constexpr int VROW = D + kVPad;
   static_assert(NH == 2, "the P.V row order assumes two 16-row blocks");
   const int lr = lane & 15, lq = lane >> 4, rg = lane / LPR, c = lane % LPR;
-  // K load li of lane group lq holds elements 32*KPL*li + EPL*lq .. + EPL-1,
-  // the A operands of k-steps KPL*li .. KPL*li + KPL-1 (the queries use the
-  // same element order; q.k does not depend on it).
-  typename KV::Raw kr[NH][NK / KPL];
-#pragma unroll
-  for (int h = 0; h < NH; ++h) {
-    const int r = rs + 16 * h + lr;
-    const int wpos = has_win ? __shfl(pos_l, 16 * h + lr, 64) : 0;
-    int cr = 0;  // rows past the tile end read row 0 and get weight 0
-    if (r < re) cr = has_win ? a.Lp + wpos : r;
-#pragma unroll
-    for (int li = 0; li < NK / KPL; ++li)
-      kr[h][li] = KV::load(kmf + cr * a.sr + 32 * KPL * KV::kBytes * li);
-  }
-  typename KV::Raw vr[UV];
-#pragma unroll
-  for (int u = 0; u < UV; ++u) {
-    const int r = rs + u * RPI + rg;
-    const int wpos = has_win ? __shfl(pos_l, u * RPI + rg, 64) : 0;
-    int cr = 0;
-    if (r < re) cr = has_win ? a.Lp + wpos : r;
-    vr[u] = KV::load(vb + cr * a.sr);
-  }
+  const auto& kr = raw.k;
+  const auto& vr = raw.v;
   f32x4 sc[NH];
 #pragma unroll
   for (int h = 0; h < NH; ++h) {
@@ -479,6 +499,15 @@ __device__ __forceinline__ void mfma_tile(const DecodeArgs& a, int lane, int rs,
   fence_wave();  // the next tile rewrites the V tile
 }
 
+// Dynamic LDS of an MFMA-tile workgroup of nw waves: the V tiles, reused
+// for the per-wave partial results (a multiple of 16 bytes).
+template <int D, int G>
+__host__ __device__ constexpr uint32_t mf_lds_bytes(int nw) {
+  const uint32_t vt = static_cast<uint32_t>(nw) * kMfmaTile * (D + kVPad) * 2;
+  const uint32_t red = static_cast<uint32_t>(nw) * G * (D + 2) * 4;
+  return ((vt > red ? vt : red) + 15u) & ~15u;
+}
+
 template <class KV, int D, int G, int U, bool FUSED, bool MF>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   constexpr int EPL = KV::kEpl;    // elements a lane loads per 16-byte access
@@ -491,20 +520,22 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   static_assert(T <= 64, "one kept position per lane");
   static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
   constexpr int KS = FUSED ? max_fused_split(MF) : 1;
-  // The per-wave partial results (red) and, in the MFMA tile, the per-wave
-  // V tiles share one LDS block: the V tiles are dead once every wave has
-  // left the tile loop.
-  constexpr int NWMAX = MF ? kWavesMfma : kWaves;  // waves of a workgroup at most
-  constexpr int kRedBytes = NWMAX * G * (D + 2) * 4;
-  constexpr int kVtBytes = MF ? NWMAX * kMfmaTile * (D + kVPad) * 2 : 0;
-  __shared__ __attribute__((aligned(16)))
-  unsigned char smem[kRedBytes > kVtBytes ? kRedBytes : kVtBytes];
-  float (*red)[G][D + 2] = reinterpret_cast<float (*)[G][D + 2]>(smem);
+  // The per-wave partial results (red): static LDS on the vector-ALU tile.
+  // The MFMA tile keeps them in its dynamic LDS block (sized for the
+  // launch's waves, mf_lds_bytes), where they reuse the per-wave V tiles,
+  // dead once every wave has left the tile loop.  The fused step's skip
+  // bitmaps (one per wave) follow in dynamic LDS.
+  constexpr int kRedBytes = MF ? 16 : kWaves * G * (D + 2) * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kRedBytes];
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_lds[];
+  const int nw_launch = blockDim.x >> 6;
+  const uint32_t mf_bytes = MF ? mf_lds_bytes<D, G>(nw_launch) : 0u;
+  float (*red)[G][D + 2] = reinterpret_cast<float (*)[G][D + 2]>(MF ? dyn_lds : smem);
   __shared__ float wl_s[G][KS];    // fused: window logits of the split
   __shared__ int kp_s[KS];         // fused: kept positions of the split
   // MF: one V tile per wave (bf16, rows padded), read back transposed
-  uint16_t* vt_w = reinterpret_cast<uint16_t*>(smem) + (threadIdx.x >> 6) * kMfmaTile * (D + kVPad);
-  extern __shared__ uint32_t bm_all[];  // fused: one skip bitmap per wave
+  uint16_t* vt_w = reinterpret_cast<uint16_t*>(dyn_lds) + (threadIdx.x >> 6) * kMfmaTile * (D + kVPad);
+  uint32_t* bm_all = reinterpret_cast<uint32_t*>(dyn_lds + mf_bytes);
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -546,15 +577,29 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   constexpr bool kScaled = KV::kBytes == 1;
   const float ks_raw = kScaled ? *(a.ks ? a.ks + pair : reinterpret_cast<const float*>(a.q)) : 1.f;
   const float vs_raw = kScaled ? *(a.vs ? a.vs + pair : reinterpret_cast<const float*>(a.q)) : 1.f;
+  // Tiles of the split from its rows alone: the prompt tiles of an active
+  // request (p0) and the most window tiles (wmax).  The wave-to-tile
+  // mapping depends on these and not on the request's length, so the waves
+  // that may rank window rows are known before the position arrives.  The
+  // vector-ALU tile deals the tiles round robin; the MFMA tile gives each
+  // wave a block of `per` consecutive tiles (prompt tiles first), so a wave
+  // of prompt tiles issues its loads without waiting for a ranking.
+  const int pe0 = min(r0 + a.C, a.Lp);
+  const int p0 = pe0 > r0 ? (pe0 - r0 + T - 1) / T : 0;
+  const int ws0 = max(r0, a.Lp);
+  const int wmax = r0 + a.C > ws0 ? (r0 + a.C - ws0 + T - 1) / T : 0;
+  const int per = MF ? (p0 + wmax + nwaves - 1) / nwaves : 0;
   StateRegs sreg{};
   sreg.cnt = has_state ? cnt_raw : 0;
   if constexpr (FUSED) {
-    const int pe0 = min(r0 + a.C, a.Lp);
-    const int p0 = pe0 > r0 ? (pe0 - r0 + T - 1) / T : 0;  // prompt tiles of an active request
-    const int ws0 = max(r0, a.Lp);
-    const int wmax = r0 + a.C > ws0 ? (r0 + a.C - ws0 + T - 1) / T : 0;  // most window tiles
-    const int j0 = p0 + ((wave - p0) % nwaves + nwaves) % nwaves;
-    load_state(a, pair, lane, has_state && j0 < p0 + wmax, sreg);
+    bool may_rank;
+    if (per > 0) {
+      const int jb0 = wave * per;
+      may_rank = max(jb0, p0) < min(jb0 + per, p0 + wmax);
+    } else {
+      may_rank = p0 + ((wave - p0) % nwaves + nwaves) % nwaves < p0 + wmax;
+    }
+    load_state(a, pair, lane, has_state && may_rank, sreg);
   }
   // Settle the scalar values here, all at once: left alone, the compiler
   // sinks each load to its first use and waits for them one at a time.
@@ -622,18 +667,63 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   // reports the plan's count and flags, as dsa_plan would.
   bool reporter = false;
   int rep_flags = 0;
-  if constexpr (FUSED) {
-    // First window tile of this wave, if it has one.
-    const int j0 = P + ((wave - P) % nwaves + nwaves) % nwaves;
-    reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && j0 == P);
+  // The wave's tiles: j = jb, jb + js, ... below je (see p0 and per; an
+  // active request has P == p0 and at most wmax window tiles).
+  const int ntile = P + Wn;
+  int jb = wave, je = ntile, js = nwaves;
+  if (per > 0) {
+    jb = min(wave * per, ntile);
+    je = min(jb + per, ntile);
+    js = 1;
   }
+  // First window tile of the wave (it has one if jw0 < je).
+  const int jw0 = js == 1 ? max(jb, P) : P + ((wave - P) % nwaves + nwaves) % nwaves;
+  if constexpr (FUSED)
+    reporter = rr.t < 0 ? (s == 0 && wave == 0) : (w0 == 0 && Wn > 0 && jw0 == P && jw0 < je);
 
-  // Fused step: a wave whose first tile holds prompt rows issues that tile's
-  // K loads before the ranking below, so they are in flight while the window
-  // rows are ranked (V too would not fit in 128 registers).
+  // Rows [rs, re) of tile j of the split and, for a window tile, the kept
+  // position of row rs + i in lane i (after the ranking, for the fused step).
+  struct TileRows {
+    int rs, re;
+    bool has_win;
+    int pos_l;
+  };
+  auto rows_of = [&](int j) {
+    TileRows tr;
+    const bool dec = j >= P;
+    tr.has_win = dec && !dense;
+    tr.rs = dec ? wst + (j - P) * T : r0 + j * T;
+    tr.re = min(tr.rs + T, dec ? r1 : pe);
+    tr.pos_l = 0;
+    if (tr.has_win) {
+      if constexpr (FUSED) {
+        if (lane < tr.re - tr.rs) tr.pos_l = kp_s[tr.rs + lane - a.Lp - w0];
+      } else {
+        if (lane < tr.re - tr.rs) tr.pos_l = min(max(widx[tr.rs + lane], 0), rr.t);
+      }
+      if (a.ring && tr.pos_l >= a.Ns) {  // ring slot: (pos - S) mod ring, after the S sinks
+        // kept positions lie in (t - ring, t], so one conditional add
+        // reduces them from the lap of t (a position outside that range
+        // only comes from a corrupt plan: it reads slot 0)
+        int sl = tr.pos_l - a.Ns - ring_lap;
+        if (sl < 0) sl += a.ring;
+        tr.pos_l = a.Ns + max(sl, 0);
+      }
+    }
+    return tr;
+  };
+
+  // Fused step, vector-ALU tile: a wave whose first tile holds prompt rows
+  // issues that tile's K loads before the ranking below, so they are in
+  // flight while the window rows are ranked (V too would not fit in 128
+  // registers).  The MFMA tile ranks first: its waves of prompt tiles have
+  // nothing to rank, and a wave that issued a tile's loads ahead of its
+  // ranking would stall at issue behind the CU's full memory queue and rank
+  // late.
   constexpr bool kHoist = FUSED && !MF;
   typename KV::Raw kr[UU], vr[UU];  // the vector-ALU tile's K/V
   const bool pre = kHoist && wave < P;
+  MfRaw<KV, D> ra, rb;  // the MFMA tile's K/V: two tiles in flight
   if constexpr (kHoist) {
     if (pre) {
       const int rs = r0 + wave * T;
@@ -649,14 +739,13 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   if constexpr (FUSED) {
     // Each wave ranks the kept window rows of its own tiles (its own skip
     // bitmap, its own slice of kp_s).
-    for (int j = wave; j < P + Wn; j += nwaves) {
-      if (j < P) continue;
+    if (jw0 < je) {
+      build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
+      have_set = true;
+    }
+    for (int j = jw0; j < je; j += js) {
       const int rs = wst + (j - P) * T;
       const int re = min(rs + T, r1);
-      if (!have_set) {
-        build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
-        have_set = true;
-      }
       rank_window(a, pair, lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
     }
     // The reporting wave settles the plan flags now, so the skip set is not
@@ -707,35 +796,12 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
 #pragma unroll
   for (int cb = 0; cb < (MF ? D / 16 : 1); ++cb) oacc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // One tile of the wave (tile j of the split).  hoisted: its K rows were
-  // loaded before the ranking.
+  // One vector-ALU tile of the wave (tile j of the split).  hoisted: its K
+  // rows were loaded before the ranking.
   auto tile = [&](int j, bool hoisted) {
-    const bool dec = j >= P;
-    const bool has_win = dec && !dense;
-    const int rs = dec ? wst + (j - P) * T : r0 + j * T;
-    const int re = min(rs + T, dec ? r1 : pe);
-    // Kept positions of a window tile: lane i holds row rs + i.
-    int pos_l = 0;
-    if (has_win) {
-      if constexpr (FUSED) {
-        if (lane < re - rs) pos_l = kp_s[rs + lane - a.Lp - w0];
-      } else {
-        if (lane < re - rs) pos_l = min(max(widx[rs + lane], 0), rr.t);
-      }
-      if (a.ring && pos_l >= a.Ns) {  // ring slot: (pos - S) mod ring, after the S sinks
-        // kept positions lie in (t - ring, t], so one conditional add
-        // reduces them from the lap of t (a position outside that range
-        // only comes from a corrupt plan: it reads slot 0)
-        int sl = pos_l - a.Ns - ring_lap;
-        if (sl < 0) sl += a.ring;
-        pos_l = a.Ns + max(sl, 0);
-      }
-    }
-    if constexpr (MF) {
-      mfma_tile<KV, D, G, FUSED>(a, lane, rs, re, has_win, pos_l, kmf, vb, qb, b, kvh, w0, sl,
-                                 sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
-      return;
-    }
+    const TileRows tr = rows_of(j);
+    const int rs = tr.rs, re = tr.re, pos_l = tr.pos_l;
+    const bool has_win = tr.has_win;
 #pragma unroll
     for (int u = 0; u < UU; ++u) {
       const int r = rs + u * RPI + rg;
@@ -808,20 +874,42 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       }
     }
   };
-  // A wave with hoisted K loads runs its first tile outside the loop, so the
-  // loop's registers never overlap loads still in flight.
-  int j = wave;
-  if (kHoist && pre) {
-    tile(j, true);
-    j += nwaves;
+  if constexpr (MF) {
+    // The wave's tiles two at a time: tiles j and j + nwaves are both in
+    // flight before either is computed (each branch is straight-line code,
+    // so the wait for the first tile does not also wait for the second).
+    auto compute = [&](const TileRows& tr, const MfRaw<KV, D>& raw) {
+      mf_compute<KV, D, G, FUSED>(a, lane, tr.rs, tr.re, tr.has_win, raw, qb, b, kvh, w0, sl,
+                                  sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
+    };
+    for (int j = jb; j < je; j += 2 * js) {
+      const TileRows ta = rows_of(j);
+      mf_load<KV, D>(a, lane, ta.rs, ta.re, ta.has_win, ta.pos_l, kmf, vb, ra);
+      const int j2 = j + js;
+      if (j2 < je) {
+        const TileRows tb = rows_of(j2);
+        mf_load<KV, D>(a, lane, tb.rs, tb.re, tb.has_win, tb.pos_l, kmf, vb, rb);
+        compute(ta, ra);
+        compute(tb, rb);
+      } else {
+        compute(ta, ra);
+      }
+    }
+  } else {
+    // A wave with hoisted K loads runs its first tile outside the loop, so
+    // the loop's registers never overlap loads still in flight.
+    int j = wave;
+    if (kHoist && pre) {
+      tile(j, true);
+      j += nwaves;
+    }
+    for (; j < P + Wn; j += nwaves) tile(j, false);
   }
-  for (; j < P + Wn; j += nwaves) tile(j, false);
 
   if constexpr (FUSED) {
     // The plan rows of this wave's window tiles, from the ranks in LDS.
     int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
-    for (int jw = wave; jw < P + Wn; jw += nwaves) {
-      if (jw < P) continue;
+    for (int jw = jw0; jw < je; jw += js) {
       const int rs = wst + (jw - P) * T;
       const int re = min(rs + T, r1);
       if (lane < re - rs) plan[rs - a.Lp + lane] = kp_s[rs - a.Lp + lane - w0];
@@ -899,19 +987,32 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       }
     }
   }
-  if (wave != 0) return;
-
-  // Merge the waves; lane j handles columns j and j + 64.
+  // Merge the waves: wave w takes query heads w, w + nwaves, ... of the
+  // group, and lane j columns j and j + 64.  Every LDS read of a head is
+  // issued before the first is used (the waves are added in order).
+  constexpr int NWM = MF ? kWavesMfma : kWaves;  // waves of a workgroup at most
+  for (int g = wave; g < G; g += nwaves) {
+    float mw[NWM], lw[NWM], a0[NWM], a1[NWM];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+    for (int w = 0; w < NWM; ++w) {
+      const bool ok = w < nwaves;
+      mw[w] = ok ? red[w][g][D] : kNegBig;
+      lw[w] = ok ? red[w][g][D + 1] : 0.f;
+      a0[w] = ok ? red[w][g][lane] : 0.f;
+      a1[w] = (ok && D == 128) ? red[w][g][(lane + 64) % D] : 0.f;
+    }
     float M = kNegBig;
-    for (int w = 0; w < nwaves; ++w) M = fmaxf(M, red[w][g][D]);
+#pragma unroll
+    for (int w = 0; w < NWM; ++w) M = fmaxf(M, mw[w]);
     float L = 0.f, A0 = 0.f, A1 = 0.f;
-    for (int w = 0; w < nwaves; ++w) {
-      const float sw = fast_exp2(red[w][g][D] - M);
-      L = fmaf(red[w][g][D + 1], sw, L);
-      A0 = fmaf(red[w][g][lane], sw, A0);
-      if constexpr (D == 128) A1 = fmaf(red[w][g][lane + 64], sw, A1);
+#pragma unroll
+    for (int w = 0; w < NWM; ++w) {
+      if (w < nwaves) {
+        const float sw = fast_exp2(mw[w] - M);
+        L = fmaf(lw[w], sw, L);
+        A0 = fmaf(a0[w], sw, A0);
+        if constexpr (D == 128) A1 = fmaf(a1[w], sw, A1);
+      }
     }
     const int h = kvh * G + g;
     if (nsplit <= 1) {
@@ -941,11 +1042,10 @@ void decode_kernel(DecodeArgs a) {
   decode_body<KV, D, G, U, FUSED, false>(a);
 }
 
-// The grouped-head (MFMA) tile holds K and V of 32 rows and the output
-// blocks in registers; the occupancy floor keeps three waves per SIMD
-// resident.
+// The grouped-head (MFMA) tile holds K and V of two 32-row tiles and the
+// output blocks in registers (up to 256 of them: two waves per SIMD).
 template <class KV, int D, int G, bool FUSED>
-__global__ __launch_bounds__(64 * kWavesMfma) __attribute__((amdgpu_waves_per_eu(3, 8)))
+__global__ __launch_bounds__(64 * kWavesMfma) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void decode_mfma_kernel(DecodeArgs a) {
   decode_body<KV, D, G, 2, FUSED, true>(a);
 }
@@ -1060,7 +1160,8 @@ void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEven
   const int grid = d.B * d.Hkv * d.S;
   const int nw = KV::kBytes == 1 ? d.NW_fp8 : d.NW;
   const int block = 64 * nw;
-  const uint32_t lds = FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u;
+  const uint32_t lds = (MF ? mf_lds_bytes<D, G>(nw) : 0u) +
+                       (FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u);
   if constexpr (MF) {
     if (t0 || t1)
       hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED>, dim3(grid), dim3(block), lds, st,

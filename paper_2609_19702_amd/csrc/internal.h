@@ -41,7 +41,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_SPLIT_KB 192  // K+V bytes per split workgroup, sparse modes, vector-ALU tile
 #endif
 #ifndef DSA_TUNE_SPLIT_KB_MFMA
-#define DSA_TUNE_SPLIT_KB_MFMA 96  // the same for the grouped-head MFMA tile
+#define DSA_TUNE_SPLIT_KB_MFMA 256  // the same for the grouped-head MFMA tile
 #endif
 #ifndef DSA_TUNE_SPLIT_KB_DENSE_64
 #define DSA_TUNE_SPLIT_KB_DENSE_64 24  // dense mode, d = 64, one query head per KV head
@@ -50,7 +50,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_SPLIT_KB_DENSE_128 96  // dense mode, d = 128, one query head per KV head
 #endif
 #ifndef DSA_TUNE_SPLIT_KB_DENSE_MFMA
-#define DSA_TUNE_SPLIT_KB_DENSE_MFMA 256  // dense mode, grouped query heads
+#define DSA_TUNE_SPLIT_KB_DENSE_MFMA 128  // dense mode, grouped query heads
 #endif
 #ifndef DSA_TUNE_MIN_WGS
 #define DSA_TUNE_MIN_WGS 512  // split further while a launch has fewer workgroups (dense mode)
@@ -63,7 +63,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
                                       // their logits and positions in LDS), vector-ALU tile
 #endif
 #ifndef DSA_TUNE_MAX_FUSED_SPLIT_MFMA
-#define DSA_TUNE_MAX_FUSED_SPLIT_MFMA 256  // the same for the MFMA tile (its V tiles also use LDS)
+#define DSA_TUNE_MAX_FUSED_SPLIT_MFMA 512  // the same for the MFMA tile
 #endif
 #ifndef DSA_TUNE_UNROLL
 #define DSA_TUNE_UNROLL 0  // loads in flight per wave (2, 4 or 8); 0: by group size
@@ -76,7 +76,10 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_VALU_WAVES 4  // most waves per workgroup of the vector-ALU decode tile
 #endif
 #ifndef DSA_TUNE_MFMA_WAVES
-#define DSA_TUNE_MFMA_WAVES 4  // most waves per workgroup of the grouped-head MFMA tile
+#define DSA_TUNE_MFMA_WAVES 8  // most waves per workgroup of the grouped-head MFMA tile
+#endif
+#ifndef DSA_TUNE_MFMA_WAVES_DENSE
+#define DSA_TUNE_MFMA_WAVES_DENSE 2  // the same in dense mode (long rows, many workgroups)
 #endif
 #ifndef DSA_TUNE_VALU_GQA
 #define DSA_TUNE_VALU_GQA 0  // 1: grouped query heads on the vector-ALU tile instead of MFMA
@@ -86,8 +89,10 @@ constexpr int kWaves = 4;          // waves per workgroup (the MFMA decode tile:
 constexpr int kBlock = 64 * kWaves;
 constexpr int kWavesMfma = DSA_TUNE_MFMA_WAVES;
 constexpr int kWavesValu = DSA_TUNE_VALU_WAVES;
+constexpr int kWavesMfmaDense = DSA_TUNE_MFMA_WAVES_DENSE;
 static_assert(kWavesValu >= 1 && kWavesValu <= kWaves, "vector-ALU workgroup waves");
 static_assert(kWavesMfma >= 1 && kWavesMfma <= 16, "MFMA workgroup waves");
+static_assert(kWavesMfmaDense >= 1 && kWavesMfmaDense <= kWavesMfma, "MFMA workgroup waves");
 constexpr int kMfmaTile = 32;        // rows per wave tile of the MFMA (grouped-head) path
 constexpr int kMaxFusedSplit = DSA_TUNE_MAX_FUSED_SPLIT;
 constexpr int kMaxFusedSplitMfma = DSA_TUNE_MAX_FUSED_SPLIT_MFMA;

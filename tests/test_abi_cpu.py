@@ -124,7 +124,7 @@ def test_layouts_and_split_config(mode, sinks, shape, par):
     rows_max = p.prompt_len + (pl.cap if mode else L_dec)
     block = 32 if li.kernel_variant == 100 else (512 // s.head_dim) * li.kernel_variant
     assert (li.kernel_variant == 100) == (s.num_q_heads > s.num_kv_heads)
-    assert 1 <= li.waves_per_group <= 4
+    assert 1 <= li.waves_per_group <= (8 if li.kernel_variant == 100 else 4)
     assert li.rows_per_split % block == 0
     assert li.rows_per_split * li.max_splits >= rows_max
     assert li.rows_per_split * (li.max_splits - 1) < max(rows_max, 1)
@@ -180,8 +180,8 @@ BENCH_CONFIGS = {
     ("llamagen_xl", 0): (128, 6, 7680, 3, 8),
     ("janus_pro_7b", 1): (288, 1, 4096, 4, 8),
     ("janus_pro_7b", 0): (192, 5, 20480, 4, 8),
-    ("emu3_8b_gqa", 1): (160, 3, 768, 4, 100),
-    ("emu3_8b_gqa", 0): (512, 9, 2304, 4, 100),
+    ("emu3_8b_gqa", 1): (480, 1, 256, 8, 100),
+    ("emu3_8b_gqa", 0): (256, 17, 4352, 2, 100),
 }
 
 
