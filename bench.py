@@ -570,8 +570,9 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-            "kernel": ("decode_kernel + combine_select_kernel (fused step, one interval)"
-                       if info.max_splits > 1 else "decode_kernel (fused step)"),
+            "kernel": ((("decode_mfma_kernel" if info.kernel_variant == 100 else "decode_kernel")
+                        + (" + combine_select_kernel (fused step, one interval)"
+                           if info.max_splits > 1 else " (fused step)"))),
             "bytes_per_launch": per_launch,
             "launches_timed": len(launch_sparse),
             "launch_timing": "eager" if args.eager else "eager_back_to_back",
