@@ -69,9 +69,10 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #define DSA_TUNE_UNROLL 0  // loads in flight per wave (2, 4 or 8); 0: by group size
 #endif
 #ifndef DSA_TUNE_UNROLL_FP8
-#define DSA_TUNE_UNROLL_FP8 6  // loads in flight per wave and operand on fp8 caches, at most
-#endif                         // (8 spills registers at d = 128: 73 us against 59 us per
-                               // Janus-like layer; 4 gives 61 us)
+#define DSA_TUNE_UNROLL_FP8 5  // loads in flight per wave and operand on fp8 caches, at most
+#endif                         // (d = 128: 40-row tiles, eight per Janus-like request, two per
+                               // wave: 55.5 us per layer against 56.8 us with 6 and 57.8 us
+                               // with 7; 8 spills registers)
 #ifndef DSA_TUNE_VALU_WAVES
 #define DSA_TUNE_VALU_WAVES 4  // most waves per workgroup of the vector-ALU decode tile
 #endif
