@@ -875,9 +875,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     }
   };
   if constexpr (MF) {
-    // The wave's tiles two at a time: tiles j and j + nwaves are both in
-    // flight before either is computed (each branch is straight-line code,
-    // so the wait for the first tile does not also wait for the second).
+    // The wave's block of tiles two at a time: tiles j and j + 1 are both
+    // in flight before either is computed (each branch is straight-line
+    // code, so the wait for the first tile does not also wait for the
+    // second).
     auto compute = [&](const TileRows& tr, const MfRaw<KV, D>& raw) {
       mf_compute<KV, D, G, FUSED>(a, lane, tr.rs, tr.re, tr.has_win, raw, qb, b, kvh, w0, sl,
                                   sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
