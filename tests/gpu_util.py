@@ -11,6 +11,7 @@ import numpy as np
 import torch
 
 from oracle import alg1
+from oracle import fp8 as ofp8
 from oracle.tieband import dot_band, logit_band, within_tie_band  # noqa: F401
 from paper_2609_19702_amd import binding as B
 
@@ -74,6 +75,18 @@ def request_arrays(kv, b, Lp):
     """fp64 (Kp, Vp, K, V) of request b from a head-major bf16 cache."""
     k = kv.k[b].to(torch.float64).cpu().numpy()
     v = kv.v[b].to(torch.float64).cpu().numpy()
+    return k[:, :Lp], v[:, :Lp], k[:, Lp:], v[:, Lp:]
+
+
+def fp8_request_arrays(kv, b, Lp, Hkv):
+    """fp64 (Kp, Vp, K, V) of request b of an fp8 cache, decoded and scaled
+    by the oracle."""
+    kc = kv.k[b].cpu().numpy()
+    vc = kv.v[b].cpu().numpy()
+    ks = kv.k_scale.cpu().numpy()[b * Hkv:(b + 1) * Hkv]
+    vs = kv.v_scale.cpu().numpy()[b * Hkv:(b + 1) * Hkv]
+    k = np.stack([ofp8.dequantize(kc[h], ks[h]) for h in range(Hkv)])
+    v = np.stack([ofp8.dequantize(vc[h], vs[h]) for h in range(Hkv)])
     return k[:, :Lp], v[:, :Lp], k[:, Lp:], v[:, Lp:]
 
 

@@ -24,21 +24,10 @@ from oracle import fp8 as ofp8
 from oracle import step as ostep
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import (DEV, TOL, check_layer_vs_oracle, dot_band, offsets_from_buffer, rel_err,
-                            say, states_to_buffer, within_tie_band)
+from tests.gpu_util import (DEV, TOL, check_layer_vs_oracle, dot_band, fp8_request_arrays,
+                            offsets_from_buffer, rel_err, say, states_to_buffer, within_tie_band)
 
 pytestmark = pytest.mark.gpu
-
-
-def fp8_request_arrays(kv, b, Lp, Hkv):
-    """fp64 (Kp, Vp, K, V) of request b, decoded and scaled by the oracle."""
-    kc = kv.k[b].cpu().numpy()
-    vc = kv.v[b].cpu().numpy()
-    ks = kv.k_scale.cpu().numpy()[b * Hkv:(b + 1) * Hkv]
-    vs = kv.v_scale.cpu().numpy()[b * Hkv:(b + 1) * Hkv]
-    k = np.stack([ofp8.dequantize(kc[h], ks[h]) for h in range(Hkv)])
-    v = np.stack([ofp8.dequantize(vc[h], vs[h]) for h in range(Hkv)])
-    return k[:, :Lp], v[:, :Lp], k[:, Lp:], v[:, Lp:]
 
 
 @pytest.mark.parametrize("Hq,Hkv,d", [(1, 1, 64), (1, 1, 128), (2, 1, 64), (4, 1, 128)])

@@ -13,7 +13,7 @@ that a split has
 * 17 tiles on 8 waves (blocks of three: a pair, then a single tile),
 
 and, in dense mode, splits of eight tiles on two waves (two pairs per
-wave).  Positions cover an unused slot, the first decode steps (fewer kept
+wave); two of the cases also over fp8 caches.  Positions cover an unused slot, the first decode steps (fewer kept
 rows than N_att, so some waves get no tile), every phase boundary of
 Algorithm 1 and ragged ones.  Kept sets must match bit for bit, outputs
 within the tolerance and every phase-2 pick the oracle's argmin or a
@@ -27,8 +27,8 @@ import torch
 
 from paper_2609_19702_amd import binding as B
 from paper_2609_19702_amd import synth
-from tests.gpu_util import (DEV, c_replay_states, check_layer_vs_oracle, request_arrays, say,
-                            states_to_buffer)
+from tests.gpu_util import (DEV, c_replay_states, check_layer_vs_oracle, fp8_request_arrays,
+                            request_arrays, say, states_to_buffer)
 
 pytestmark = pytest.mark.gpu
 
@@ -49,11 +49,11 @@ def positions(Bn, L, N_r, N_att, seed):
     return (fixed + [rng.randrange(L) for _ in range(Bn - len(fixed))])[:Bn]
 
 
-def run(p, s, q, kv, pos, st, fused):
+def run(p, s, q, kv, pos, st, fused, lay=None):
     bufs = B.alloc_buffers(p, s, DEV)
     st = st.clone() if st is not None else None
     scale = 1 / math.sqrt(s.head_dim)
-    lay = B.kv_layout(kv.k)
+    lay = B.kv_layout(kv.k) if lay is None else lay
     sparse = p.mode != B.MODE_DENSE
     if fused:
         B.decode_step(p, s, q, kv.k, kv.v, lay, pos, st, bufs.plan, scale, bufs.out, bufs.logits,
@@ -94,6 +94,34 @@ def test_mfma_tile_mapping_matches_oracle(case, fused):
     arrays = [request_arrays(kv, b, Lp) for b in range(Bn)]
     forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, bufs.plan, bufs.out, st,
                                    bufs.logits)
+    say(f"  near-tie picks adopted: {forced}")
+    assert forced <= 2
+
+
+@pytest.mark.parametrize("case", CASES[1:3], ids=[c[0] for c in CASES[1:3]])
+def test_mfma_tile_mapping_fp8(case):
+    """The same mapping over fp8 (E4M3) caches with per-(request, KV head)
+    scales: two k-steps per 16-byte K load and half the V registers per
+    tile, fused step."""
+    name, Bn, Hq, Hkv, d, Lp, grid, N_r, N_att, tiles = case
+    L = grid * grid
+    p = B.make_params(Lp, grid, grid, N_r, N_att)
+    s = B.make_shape(Bn, Hq, Hkv, d)
+    info = B.launch_info(p, s)
+    assert info.kernel_variant == 100 and info.max_splits == 1
+    say("mfma tiles fp8", name, "waves", info.waves_per_group)
+    ts = positions(Bn, L, N_r, N_att, seed=tiles + 1)
+    rng = random.Random(tiles * 37 + Hkv)
+    w = synth.Workload(name, 1, Bn, Hq, Hkv, d, Lp, grid, grid, N_r, outlier_frac=0.01)
+    kv = synth.to_fp8(synth.layer_kv(w, 0, DEV))
+    q = synth.layer_query(w, 0, DEV)
+    states, _ = c_replay_states(N_r, N_att, L, ts, Hkv, rng)
+    st0 = states_to_buffer(p, s, states, ts)
+    pos = torch.tensor(ts, dtype=torch.int32, device=DEV)
+    lay = B.kv_layout(kv.k, k_scale=kv.k_scale, v_scale=kv.v_scale)
+    bufs, st = run(p, s, q, kv, pos, st0, True, lay)
+    arrays = [fp8_request_arrays(kv, b, Lp, Hkv) for b in range(Bn)]
+    forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, bufs.plan, bufs.out, st)
     say(f"  near-tie picks adopted: {forced}")
     assert forced <= 2
 
