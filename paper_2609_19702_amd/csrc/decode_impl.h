@@ -241,8 +241,7 @@ __device__ __forceinline__ bool is_kept(const SkipSet& ss, int p) {
 // latency is paid once per batch rather than once per chunk.
 constexpr int kRankBatch = 4;
 
-__device__ void rank_window(const DecodeArgs& a, int pair, int lane, SkipSet& ss, int lo, int hi,
-                            int* kp, int kp_base) {
+__device__ void rank_window(int lane, SkipSet& ss, int lo, int hi, int* kp, int kp_base) {
   const uint64_t below = (uint64_t(1) << lane) - 1;
   for (int r = lo + lane; r < min(hi, ss.sk); r += 64)  // sink rank r is position r
     kp[r - kp_base] = r;
@@ -662,7 +661,6 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int Wn = r1 > wst ? (r1 - wst + T - 1) / T : 0;
 
   SkipSet ss{};
-  bool have_set = false;
   // The wave holding window rank 0 (the first decode tile of the pair)
   // reports the plan's count and flags, as dsa_plan would.
   bool reporter = false;
@@ -741,12 +739,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     // bitmap, its own slice of kp_s).
     if (jw0 < je) {
       build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
-      have_set = true;
     }
     for (int j = jw0; j < je; j += js) {
       const int rs = wst + (j - P) * T;
       const int re = min(rs + T, r1);
-      rank_window(a, pair, lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
+      rank_window(lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
     }
     // The reporting wave settles the plan flags now, so the skip set is not
     // live through the K/V loop.

@@ -139,7 +139,7 @@ hipError_t launch_plan(const Derived& d, const PlanArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_reset(const Derived& d, const ResetArgs& a, hipStream_t st) {
+hipError_t launch_reset(const Derived& /*d*/, const ResetArgs& a, hipStream_t st) {
   const int grid = (a.pairs + 255) / 256;
   reset_kernel<<<grid, 256, 0, st>>>(a);
   return hipGetLastError();
