@@ -379,10 +379,10 @@ __device__ __forceinline__ void mf_load(const DecodeArgs& a, int lane, int rs, i
 // accumulates in the C layout (lane l: heads 4*(l/16) + r, column l%16 of
 // the block).  Each weight is split into two bf16 terms (hi + lo, relative
 // error about 2^-17) so the product keeps fp32-level accuracy.
-template <class KV, int D, int G, bool FUSED>
+template <class KV, int D, int G>
 __device__ __forceinline__ void mf_compute(const DecodeArgs& a, int lane, int rs, int re,
                                            bool has_win, const MfRaw<KV, D>& raw,
-                                           const bf16x8* qb, int b, int kvh, int w0, float sl,
+                                           const bf16x8* qb, int w0, float sl,
                                            float sl2, float& m_c, float& l_c,
                                            f32x4 (&oacc)[D / 16], float* wls, uint16_t* vt) {
   constexpr int EPL = KV::kEpl;  // elements per 16-byte load
@@ -403,19 +403,16 @@ __device__ __forceinline__ void mf_compute(const DecodeArgs& a, int lane, int rs
       sc[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(KV::to_bf16(kr[h][i / KPL], i % KPL), qb[i],
                                                       sc[h], 0, 0, 0);
   }
+  // Window logits go to LDS; the wave copies them out after its last tile
+  // (a global store here would sit in the memory queue ahead of the waits
+  // for this tile's and the next tile's data).
   if (has_win && lr < G) {
 #pragma unroll
     for (int h = 0; h < NH; ++h)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = rs + 16 * h + 4 * lq + j;
-        if (r < re) {
-          const float logit = sc[h][j] * sl;
-          if (a.wlog)
-            a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + lr) * a.plan_cap + (r - a.Lp)] =
-                logit;
-          if constexpr (FUSED) wls[lr * kMaxFusedSplitMfma + (r - a.Lp - w0)] = logit;
-        }
+        if (r < re) wls[lr * kMaxFusedSplitMfma + (r - a.Lp - w0)] = sc[h][j] * sl;
       }
   }
   // V rows of the tile into the wave's LDS tile, as bf16 (exact for fp8).
@@ -498,13 +495,24 @@ __device__ __forceinline__ void mf_compute(const DecodeArgs& a, int lane, int rs
   fence_wave();  // the next tile rewrites the V tile
 }
 
-// Dynamic LDS of an MFMA-tile workgroup of nw waves: the V tiles, reused
-// for the per-wave partial results (a multiple of 16 bytes).
+// Dynamic LDS of the window logits of a sparse-mode split: G heads of at
+// most max_fused_split rows (a multiple of 16 bytes).
+__host__ __device__ constexpr uint32_t wl_lds_bytes(int G, bool mf) {
+  return static_cast<uint32_t>(G) * max_fused_split(mf) * 4u;
+}
+
+// Dynamic LDS of an MFMA-tile workgroup of nw waves: the V tiles, then the
+// per-wave partial results (their own space, so a wave writes its partials
+// as soon as its last tile is done, without waiting for the others).  Each
+// part is a multiple of 16 bytes.
+template <int D>
+__host__ __device__ constexpr uint32_t mf_vt_bytes(int nw) {
+  return static_cast<uint32_t>(nw) * kMfmaTile * (D + kVPad) * 2;
+}
 template <int D, int G>
 __host__ __device__ constexpr uint32_t mf_lds_bytes(int nw) {
-  const uint32_t vt = static_cast<uint32_t>(nw) * kMfmaTile * (D + kVPad) * 2;
   const uint32_t red = static_cast<uint32_t>(nw) * G * (D + 2) * 4;
-  return ((vt > red ? vt : red) + 15u) & ~15u;
+  return mf_vt_bytes<D>(nw) + ((red + 15u) & ~15u);
 }
 
 template <class KV, int D, int G, int U, bool FUSED, bool MF>
@@ -518,23 +526,26 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   constexpr int KPL = EPL / 8;     // MFMA k-steps per K load (MF only)
   static_assert(T <= 64, "one kept position per lane");
   static_assert(!MF || G >= 2, "the MFMA tile serves grouped query heads");
-  constexpr int KS = FUSED ? max_fused_split(MF) : 1;
+  constexpr int KS = max_fused_split(MF);  // window rows of a sparse-mode split at most
   // The per-wave partial results (red): static LDS on the vector-ALU tile.
   // The MFMA tile keeps them in its dynamic LDS block (sized for the
-  // launch's waves, mf_lds_bytes), where they reuse the per-wave V tiles,
-  // dead once every wave has left the tile loop.  The fused step's skip
-  // bitmaps (one per wave) follow in dynamic LDS.
+  // launch's waves, mf_lds_bytes), after the per-wave V tiles.  The fused
+  // step's skip bitmaps (one per wave) follow in dynamic LDS.
   constexpr int kRedBytes = MF ? 16 : kWaves * G * (D + 2) * 4;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kRedBytes];
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_lds[];
   const int nw_launch = blockDim.x >> 6;
   const uint32_t mf_bytes = MF ? mf_lds_bytes<D, G>(nw_launch) : 0u;
-  float (*red)[G][D + 2] = reinterpret_cast<float (*)[G][D + 2]>(MF ? dyn_lds : smem);
-  __shared__ float wl_s[G][KS];    // fused: window logits of the split
-  __shared__ int kp_s[KS];         // fused: kept positions of the split
+  float (*red)[G][D + 2] =
+      reinterpret_cast<float (*)[G][D + 2]>(MF ? dyn_lds + mf_vt_bytes<D>(nw_launch) : smem);
+  __shared__ int kp_s[FUSED ? KS : 1];  // fused: kept positions of the split
   // MF: one V tile per wave (bf16, rows padded), read back transposed
   uint16_t* vt_w = reinterpret_cast<uint16_t*>(dyn_lds) + (threadIdx.x >> 6) * kMfmaTile * (D + kVPad);
-  uint32_t* bm_all = reinterpret_cast<uint32_t*>(dyn_lds + mf_bytes);
+  // Sparse mode: the split's window logits, head g at wl_s[g * KS + rank]
+  // (dynamic LDS; none in dense mode).
+  float* wl_s = reinterpret_cast<float*>(dyn_lds + mf_bytes);
+  const uint32_t wl_bytes = a.mode != DSA_MODE_DENSE ? wl_lds_bytes(G, MF) : 0u;
+  uint32_t* bm_all = reinterpret_cast<uint32_t*>(dyn_lds + mf_bytes + wl_bytes);
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -824,19 +835,15 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
         sc[u][g] = group_sum<LPR>(x);
       }
     }
+    // Window logits go to LDS (copied out after the wave's last tile, so
+    // no global store waits ahead of this tile's V data).
     if (has_win && c == 0) {
 #pragma unroll
       for (int u = 0; u < UU; ++u) {
         const int r = rs + u * RPI + rg;
         if (r < re) {
 #pragma unroll
-          for (int g = 0; g < G; ++g) {
-            const float logit = sc[u][g] * sl;
-            if (a.wlog)
-              a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (r - a.Lp)] =
-                  logit;
-            if constexpr (FUSED) wl_s[g][r - a.Lp - w0] = logit;
-          }
+          for (int g = 0; g < G; ++g) wl_s[g * KS + (r - a.Lp - w0)] = sc[u][g] * sl;
         }
       }
     }
@@ -877,8 +884,8 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     // code, so the wait for the first tile does not also wait for the
     // second).
     auto compute = [&](const TileRows& tr, const MfRaw<KV, D>& raw) {
-      mf_compute<KV, D, G, FUSED>(a, lane, tr.rs, tr.re, tr.has_win, raw, qb, b, kvh, w0, sl,
-                                  sl2, m_c, l_c, oacc, &wl_s[0][0], vt_w);
+      mf_compute<KV, D, G>(a, lane, tr.rs, tr.re, tr.has_win, raw, qb, w0, sl, sl2, m_c, l_c,
+                           oacc, wl_s, vt_w);
     };
     for (int j = jb; j < je; j += 2 * js) {
       const TileRows ta = rows_of(j);
@@ -904,6 +911,21 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     for (; j < P + Wn; j += nwaves) tile(j, false);
   }
 
+  // The window logits of this wave's window tiles, from LDS (the wave wrote
+  // them itself), after its last wait for K/V data.
+  if (a.wlog && !dense) {
+    fence_wave();
+    for (int jw = jw0; jw < je; jw += js) {
+      const int rs = wst + (jw - P) * T;
+      const int nr = min(rs + T, r1) - rs;
+      if (lane < nr) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+          a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (rs - a.Lp + lane)] =
+              wl_s[g * KS + (rs - a.Lp - w0 + lane)];
+      }
+    }
+  }
   if constexpr (FUSED) {
     // The plan rows of this wave's window tiles, from the ranks in LDS.
     int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
@@ -919,7 +941,6 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
 
   if constexpr (MF) {
-    __syncthreads();  // every wave is done with its V tile (red aliases it)
     // Head g's running max sits in the lanes with lr == g; its sum is split
     // over the four lanes lr + 16*q.  The output is already the wave's full
     // sum in the C layout: lane l holds heads 4*(l/16) + r, column l%16 of
@@ -959,45 +980,44 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   }
   __syncthreads();
 
+  // Phase-2 selection, when this workgroup saw every kept window key (the
+  // same for every wave of the workgroup).  The sinks (the first Ns kept
+  // ranks) are never candidates.  The stored count is the one loaded at the
+  // start (only this workgroup writes it), so the selection waits for no
+  // memory.
+  bool sel = false;
+  const int ksel = rr.t - (a.Natt - 1);
+  const int nwin = n - a.Lp - a.Ns;
+  float* const wl_win = wl_s + a.Ns;  // head g's window logits at wl_win[g * KS + j]
   if constexpr (FUSED) {
-    // Phase-2 selection, when this workgroup saw every kept window key.
-    // The sinks (the first Ns kept ranks) are never candidates.
-    if (wave == nwaves - 1 && nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr + a.Ns - 2) {
-      const int k = rr.t - (a.Natt - 1);
-      if (k < a.state_cap) {
-        // The stored count as loaded at the start (only this workgroup
-        // writes it), so the selection waits for no memory.
-        const int cnt = cnt_raw;
-        if (cnt < k) {
-          if (lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
-        } else {
-          const int nwin = n - a.Lp - a.Ns;
-          const int ns = a.Ns;
-          int jbest =
-              window_argmin<G>(lane, nwin, [&](int g, int j) { return wl_s[g][ns + j]; });
-          if (lane == 0) {
-            if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-            const int d = min(max(rr.t - kp_s[ns + jbest], 0), a.Nr - 2);
-            a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
-            a.st_count[pair] = k + 1;
-          }
-        }
-      }
+    sel = nsplit == 1 && rr.t >= a.Natt - 1 && rr.t <= a.Nr + a.Ns - 2 && ksel < a.state_cap;
+    if (sel && cnt_raw < ksel) {
+      if (wave == nwaves - 1 && lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
+      sel = false;
+    }
+    // Grouped heads: each head's window softmax on a wave of its own (head
+    // g on wave nwaves - 1 - g, and so on round the waves), while the first
+    // waves merge the outputs below.
+    if constexpr (G > 1) {
+      if (sel)
+        for (int g = nwaves - 1 - wave; g < G; g += nwaves) head_terms(lane, nwin, wl_win + g * KS);
     }
   }
   // Merge the waves: wave w takes query heads w, w + nwaves, ... of the
   // group, and lane j columns j and j + 64.  Every LDS read of a head is
-  // issued before the first is used (the waves are added in order).
+  // issued before the first is used, with no branches: slots past the
+  // workgroup's waves read its last wave again (the maximum does not
+  // change) and add nothing (the waves are added in order).
   constexpr int NWM = MF ? kWavesMfma : kWaves;  // waves of a workgroup at most
   for (int g = wave; g < G; g += nwaves) {
     float mw[NWM], lw[NWM], a0[NWM], a1[NWM];
 #pragma unroll
     for (int w = 0; w < NWM; ++w) {
-      const bool ok = w < nwaves;
-      mw[w] = ok ? red[w][g][D] : kNegBig;
-      lw[w] = ok ? red[w][g][D + 1] : 0.f;
-      a0[w] = ok ? red[w][g][lane] : 0.f;
-      a1[w] = (ok && D == 128) ? red[w][g][(lane + 64) % D] : 0.f;
+      const int wr = min(w, nwaves - 1);
+      mw[w] = red[wr][g][D];
+      lw[w] = red[wr][g][D + 1];
+      a0[w] = red[wr][g][lane];
+      a1[w] = D == 128 ? red[wr][g][(lane + 64) % D] : 0.f;
     }
     float M = kNegBig;
 #pragma unroll
@@ -1005,12 +1025,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     float L = 0.f, A0 = 0.f, A1 = 0.f;
 #pragma unroll
     for (int w = 0; w < NWM; ++w) {
-      if (w < nwaves) {
-        const float sw = fast_exp2(mw[w] - M);
-        L = fmaf(lw[w], sw, L);
-        A0 = fmaf(a0[w], sw, A0);
-        if constexpr (D == 128) A1 = fmaf(a1[w], sw, A1);
-      }
+      const bool ok = w < nwaves;
+      const float sw = fast_exp2(mw[w] - M);
+      L = ok ? fmaf(lw[w], sw, L) : L;
+      A0 = ok ? fmaf(a0[w], sw, A0) : A0;
+      if constexpr (D == 128) A1 = ok ? fmaf(a1[w], sw, A1) : A1;
     }
     const int h = kvh * G + g;
     if (nsplit <= 1) {
@@ -1026,6 +1045,25 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       if (lane == 0) {
         pp[D] = M;
         pp[D + 1] = L;
+      }
+    }
+  }
+
+  if constexpr (FUSED) {
+    if constexpr (G > 1) {
+      if (sel) __syncthreads();  // every head's terms are in LDS
+    }
+    if (sel && wave == nwaves - 1) {
+      int jbest;
+      if constexpr (G > 1)
+        jbest = terms_argmin<G>(lane, nwin, [&](int g, int j) { return wl_win[g * KS + j]; });
+      else
+        jbest = window_argmin<1>(lane, nwin, [&](int, int j) { return wl_win[j]; });
+      if (lane == 0) {
+        if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
+        const int d = min(max(rr.t - kp_s[a.Ns + jbest], 0), a.Nr - 2);
+        a.st_off[static_cast<size_t>(pair) * a.state_cap + ksel] = static_cast<uint16_t>(d);
+        a.st_count[pair] = ksel + 1;
       }
     }
   }
@@ -1159,6 +1197,7 @@ void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEven
   const int nw = KV::kBytes == 1 ? d.NW_fp8 : d.NW;
   const int block = 64 * nw;
   const uint32_t lds = (MF ? mf_lds_bytes<D, G>(nw) : 0u) +
+                       (a.mode != DSA_MODE_DENSE ? wl_lds_bytes(G, MF) : 0u) +
                        (FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u);
   if constexpr (MF) {
     if (t0 || t1)

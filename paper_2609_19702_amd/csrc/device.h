@@ -146,6 +146,69 @@ __device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2)
   }
 }
 
+// The butterfly of wave_allreduce on N values at once.  Each value goes
+// through the same steps in the same order as it would alone, so the result
+// is bit for bit the same; the N exchanges of a step are independent, so a
+// wave waits for one step's latency instead of N.
+template <int N, typename Op>
+__device__ __forceinline__ void wave_allreduce_n(float (&x)[N], Op op) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dpp<kDppQuadSwap1>(x[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dpp<kDppQuadSwap2>(x[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dpp<kDppHalfMirror>(x[i]));
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(x[i], dpp<kDppRowMirror>(x[i]));
+  float a[N], b[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) xor_pair<16>(x[i], a[i], b[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(a[i], b[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) xor_pair<32>(x[i], a[i], b[i]);
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = op(a[i], b[i]);
+}
+
+// Unsigned integers in the order of the floats they come from (-0 counts as
+// +0, as a float comparison does).  Not for NaN.
+__device__ __forceinline__ uint32_t ordered_bits(float v) {
+  const uint32_t u = __float_as_uint(v + 0.f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// The smallest 64-bit key over the wave (every lane receives it).
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
+  auto take = [](uint64_t a, uint32_t lo, uint32_t hi) {
+    const uint64_t b = (static_cast<uint64_t>(hi) << 32) | lo;
+    return b < a ? b : a;
+  };
+  x = take(x, dpp_i<kDppQuadSwap1>(static_cast<int>(x)), dpp_i<kDppQuadSwap1>(static_cast<int>(x >> 32)));
+  x = take(x, dpp_i<kDppQuadSwap2>(static_cast<int>(x)), dpp_i<kDppQuadSwap2>(static_cast<int>(x >> 32)));
+  x = take(x, dpp_i<kDppHalfMirror>(static_cast<int>(x)), dpp_i<kDppHalfMirror>(static_cast<int>(x >> 32)));
+  x = take(x, dpp_i<kDppRowMirror>(static_cast<int>(x)), dpp_i<kDppRowMirror>(static_cast<int>(x >> 32)));
+  float lo0, lo1, hi0, hi1;
+  xor_pair<16>(__uint_as_float(static_cast<uint32_t>(x)), lo0, lo1);
+  xor_pair<16>(__uint_as_float(static_cast<uint32_t>(x >> 32)), hi0, hi1);
+  x = take((static_cast<uint64_t>(__float_as_uint(hi0)) << 32) | __float_as_uint(lo0),
+           __float_as_uint(lo1), __float_as_uint(hi1));
+  xor_pair<32>(__uint_as_float(static_cast<uint32_t>(x)), lo0, lo1);
+  xor_pair<32>(__uint_as_float(static_cast<uint32_t>(x >> 32)), hi0, hi1);
+  return take((static_cast<uint64_t>(__float_as_uint(hi0)) << 32) | __float_as_uint(lo0),
+              __float_as_uint(lo1), __float_as_uint(hi1));
+}
+
+// The smallest (score, index) key over the wave: a lane's best is its
+// smallest score (never NaN; +inf with index 0x7fffffff where it has no
+// candidate) and jbest its smallest index with that score, so the key order
+// gives the smallest score, then the smallest index.  Every lane returns it.
+__device__ __forceinline__ int wave_argmin_key(float best, int jbest) {
+  const uint64_t key = (static_cast<uint64_t>(ordered_bits(best)) << 32) |
+                       static_cast<uint32_t>(jbest);
+  return static_cast<int>(static_cast<uint32_t>(wave_min_u64(key)));
+}
+
 // Phase-2 selection score argmin of one KV head over its n kept window keys
 // (section 4, Algorithm 1): logit(g, j) is sm_scale * q_g . k_j of query head
 // g of the group for window key j.  Group size 1 takes the argmin of the
@@ -157,7 +220,10 @@ __device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2)
 // Windows of up to kArgminRegs * 64 keys are read once, every load issued
 // before the first use, and kept in registers for the max, sum and score
 // passes; longer windows stream the logits once per pass.  Both forms add
-// the same terms in the same order.
+// the same terms in the same order.  The group's heads go through each
+// pass side by side (their maxima and sums are reduced over the wave
+// together), and the final (score, index) minimum is one reduction of
+// packed keys.
 constexpr int kArgminRegs = 4;
 
 template <int G, typename Logit>
@@ -177,27 +243,33 @@ __device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
       for (int c = 0; c < kArgminRegs; ++c)
         if (lane + 64 * c < n) argmin_merge(best, jbest, v[0][c], lane + 64 * c);
     } else {
-      float mx[G], inv[G];
+      float mx[G], sm[G], inv[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        float m = -__builtin_inff();
+        mx[g] = -__builtin_inff();
 #pragma unroll
-        for (int c = 0; c < kArgminRegs; ++c) m = fmaxf(m, v[g][c]);
-        m = wave_max(m);
-        float s = 0.f;
-#pragma unroll
-        for (int c = 0; c < kArgminRegs; ++c)
-          if (lane + 64 * c < n) s += __expf(v[g][c] - m);
-        s = wave_sum(s);
-        mx[g] = m;
-        inv[g] = 1.f / s;
+        for (int c = 0; c < kArgminRegs; ++c) mx[g] = fmaxf(mx[g], v[g][c]);
       }
+      wave_allreduce_n<G>(mx, [](float a, float b) { return fmaxf(a, b); });
+      float e[G][kArgminRegs];  // the exponentials, computed once for both passes
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        sm[g] = 0.f;
+#pragma unroll
+        for (int c = 0; c < kArgminRegs; ++c) {
+          e[g][c] = __expf(v[g][c] - mx[g]);
+          if (lane + 64 * c < n) sm[g] += e[g][c];
+        }
+      }
+      wave_allreduce_n<G>(sm, [](float a, float b) { return a + b; });
+#pragma unroll
+      for (int g = 0; g < G; ++g) inv[g] = 1.f / sm[g];
 #pragma unroll
       for (int c = 0; c < kArgminRegs; ++c) {
         if (lane + 64 * c < n) {
           float sigma = 0.f;
 #pragma unroll
-          for (int g = 0; g < G; ++g) sigma += __expf(v[g][c] - mx[g]) * inv[g];
+          for (int g = 0; g < G; ++g) sigma += e[g][c] * inv[g];
           argmin_merge(best, jbest, sigma, lane + 64 * c);
         }
       }
@@ -205,18 +277,21 @@ __device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
   } else if constexpr (G == 1) {
     for (int j = lane; j < n; j += 64) argmin_merge(best, jbest, logit(0, j), j);
   } else {
-    float mx[G], inv[G];
+    float mx[G], sm[G], inv[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float m = -__builtin_inff();
-      for (int j = lane; j < n; j += 64) m = fmaxf(m, logit(g, j));
-      m = wave_max(m);
-      float s = 0.f;
-      for (int j = lane; j < n; j += 64) s += __expf(logit(g, j) - m);
-      s = wave_sum(s);
-      mx[g] = m;
-      inv[g] = 1.f / s;
-    }
+    for (int g = 0; g < G; ++g) mx[g] = -__builtin_inff();
+    for (int j = lane; j < n; j += 64)
+#pragma unroll
+      for (int g = 0; g < G; ++g) mx[g] = fmaxf(mx[g], logit(g, j));
+    wave_allreduce_n<G>(mx, [](float a, float b) { return fmaxf(a, b); });
+#pragma unroll
+    for (int g = 0; g < G; ++g) sm[g] = 0.f;
+    for (int j = lane; j < n; j += 64)
+#pragma unroll
+      for (int g = 0; g < G; ++g) sm[g] += __expf(logit(g, j) - mx[g]);
+    wave_allreduce_n<G>(sm, [](float a, float b) { return a + b; });
+#pragma unroll
+    for (int g = 0; g < G; ++g) inv[g] = 1.f / sm[g];
     for (int j = lane; j < n; j += 64) {
       float sigma = 0.f;
 #pragma unroll
@@ -224,12 +299,81 @@ __device__ __forceinline__ int window_argmin(int lane, int n, Logit logit) {
       argmin_merge(best, jbest, sigma, j);
     }
   }
-  // The smallest score over the wave, then the smallest index among the
-  // lanes that hold it (each lane's jbest is its smallest index with its
-  // best score, so ties still go to the smallest j).
-  const float m = wave_allreduce(best, [](float a, float b) { return fminf(a, b); });
-  const int jm = best == m ? jbest : 0x7fffffff;
-  return wave_allreduce(jm, [](int a, int b) { return min(a, b); });
+  return wave_argmin_key(best, jbest);
+}
+
+// The selection of window_argmin (G > 1) in two parts, so the heads of a
+// group can be taken by different waves of a workgroup.
+//
+// head_terms: one head's window softmax, in place: row[j] (the logit of
+// window key j, 0 <= j < n) becomes exp(row[j] - max) / sum.  The maximum,
+// the sum and the terms are the values window_argmin computes for the head
+// (same operations, same order).  Windows of up to kArgminRegs * 64 keys are
+// read into registers at once (every LDS read issued before the first use);
+// longer ones are streamed.  Called by a whole wave.
+__device__ __forceinline__ void head_terms(int lane, int n, float* row) {
+  float mx[1] = {-__builtin_inff()};
+  float sm[1] = {0.f};
+  if (n <= 64 * kArgminRegs) {
+    float v[kArgminRegs], e[kArgminRegs];
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c) {
+      const float x = row[min(lane + 64 * c, n - 1)];
+      v[c] = lane + 64 * c < n ? x : -__builtin_inff();
+    }
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c) mx[0] = fmaxf(mx[0], v[c]);
+    wave_allreduce_n<1>(mx, [](float a, float b) { return fmaxf(a, b); });
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c) {
+      e[c] = __expf(v[c] - mx[0]);
+      if (lane + 64 * c < n) sm[0] += e[c];
+    }
+    wave_allreduce_n<1>(sm, [](float a, float b) { return a + b; });
+    const float inv = 1.f / sm[0];
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c)
+      if (lane + 64 * c < n) row[lane + 64 * c] = e[c] * inv;
+    return;
+  }
+  for (int j = lane; j < n; j += 64) mx[0] = fmaxf(mx[0], row[j]);
+  wave_allreduce_n<1>(mx, [](float a, float b) { return fmaxf(a, b); });
+  for (int j = lane; j < n; j += 64) sm[0] += __expf(row[j] - mx[0]);
+  wave_allreduce_n<1>(sm, [](float a, float b) { return a + b; });
+  const float inv = 1.f / sm[0];
+  for (int j = lane; j < n; j += 64) row[j] = __expf(row[j] - mx[0]) * inv;
+}
+
+// terms_argmin: the argmin of sigma_j = sum over the group's heads g (in
+// order) of term(g, j), the terms head_terms left; the same index
+// window_argmin returns.  term(g, j) must be readable for every j < n.
+// Called by a whole wave.
+template <int G, typename Term>
+__device__ __forceinline__ int terms_argmin(int lane, int n, Term term) {
+  float best = __builtin_inff();
+  int jbest = 0x7fffffff;
+  if (n <= 64 * kArgminRegs) {
+    float t[kArgminRegs][G];
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c)
+#pragma unroll
+      for (int g = 0; g < G; ++g) t[c][g] = term(g, min(lane + 64 * c, n - 1));
+#pragma unroll
+    for (int c = 0; c < kArgminRegs; ++c) {
+      float sigma = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) sigma += t[c][g];
+      if (lane + 64 * c < n) argmin_merge(best, jbest, sigma, lane + 64 * c);
+    }
+  } else {
+    for (int j = lane; j < n; j += 64) {
+      float sigma = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) sigma += term(g, j);
+      argmin_merge(best, jbest, sigma, j);
+    }
+  }
+  return wave_argmin_key(best, jbest);
 }
 
 }  // namespace dsa
