@@ -911,29 +911,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     for (; j < P + Wn; j += nwaves) tile(j, false);
   }
 
-  // The window logits of this wave's window tiles, from LDS (the wave wrote
-  // them itself), after its last wait for K/V data.
-  if (a.wlog && !dense) {
-    fence_wave();
-    for (int jw = jw0; jw < je; jw += js) {
-      const int rs = wst + (jw - P) * T;
-      const int nr = min(rs + T, r1) - rs;
-      if (lane < nr) {
-#pragma unroll
-        for (int g = 0; g < G; ++g)
-          a.wlog[(static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + (rs - a.Lp + lane)] =
-              wl_s[g * KS + (rs - a.Lp - w0 + lane)];
-      }
-    }
-  }
   if constexpr (FUSED) {
-    // The plan rows of this wave's window tiles, from the ranks in LDS.
-    int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap;
-    for (int jw = jw0; jw < je; jw += js) {
-      const int rs = wst + (jw - P) * T;
-      const int re = min(rs + T, r1);
-      if (lane < re - rs) plan[rs - a.Lp + lane] = kp_s[rs - a.Lp + lane - w0];
-    }
     if (reporter && lane == 0) {
       a.plan_count[pair] = rr.t < 0 ? 0 : n - a.Lp;
       a.plan_flags[pair] = rep_flags;
@@ -995,12 +973,28 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       if (wave == nwaves - 1 && lane == 0) a.st_flags[pair] |= DSA_FLAG_STATE_BEHIND;
       sel = false;
     }
-    // Grouped heads: each head's window softmax on a wave of its own (head
-    // g on wave nwaves - 1 - g, and so on round the waves), while the first
-    // waves merge the outputs below.
-    if constexpr (G > 1) {
-      if (sel)
-        for (int g = nwaves - 1 - wave; g < G; g += nwaves) head_terms(lane, nwin, wl_win + g * KS);
+  }
+  // Stores of window logits and plan rows wait until every wave has left
+  // its tile loop, so none sits in the memory queue ahead of a wait for K/V
+  // data.  Head g's window logits (split ranks w0 ..) are copied out by wave
+  // nwaves - 1 - g (and so on round the waves), which then, for grouped
+  // heads, turns them into the head's window softmax for the selection,
+  // while the first waves merge the outputs below.  The last wave copies
+  // the plan rows.
+  const int nws = r1 > wst ? r1 - wst : 0;  // window rows of the split
+  for (int g = nwaves - 1 - wave; g < G; g += nwaves) {
+    if (a.wlog && !dense) {
+      float* dst = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G + g) * a.plan_cap + w0;
+      for (int i = lane; i < nws; i += 64) dst[i] = wl_s[g * KS + i];
+    }
+    if constexpr (FUSED && G > 1) {
+      if (sel) head_terms(lane, nwin, wl_win + g * KS);
+    }
+  }
+  if constexpr (FUSED) {
+    if (wave == nwaves - 1) {
+      int32_t* plan = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap + w0;
+      for (int i = lane; i < nws; i += 64) plan[i] = kp_s[i];
     }
   }
   // Merge the waves: wave w takes query heads w, w + nwaves, ... of the
