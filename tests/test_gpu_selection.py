@@ -7,6 +7,12 @@
   over the same kept keys (equal, or inside the certified fp32 tie band).
 * One query head per KV head with more than 256 kept window keys in a
   single split: the fused decode kernel runs the streaming argmin itself.
+* Grouped query heads with more than 256 kept window keys in a single split
+  (enough (request, KV head) pairs that no request is split): the fused
+  decode kernel takes the selection itself, each head's window softmax on a
+  wave of its own, then the score sum and argmin on one wave.  Checked
+  against the oracle and bit for bit against the separate calls (same plan,
+  logits, outputs and stored offsets).
 * Windows of 4096, 16384 and 20000 positions: selection states replayed by
   the literal Algorithm 1 of the C oracle (every choice random), then the
   plan's kept sets compared bit for bit with the oracle's, the outputs with
@@ -119,4 +125,42 @@ def test_large_windows_literal(window, n_att, grid, fused):
     arrays = [request_arrays(kv, b, Lp) for b in range(Bn)]
     forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, bufs.plan, bufs.out, st,
                                    bufs.logits)
+    assert forced <= 2
+
+
+SINGLE_SPLIT_GQA = [
+    # Hq, Hkv, d, L_p, grid, N_r, N_att, copies of the four positions
+    (64, 32, 128, 16, 30, 700, 400, 2),    # G = 2
+    (128, 32, 64, 16, 30, 700, 300, 2),    # G = 4
+    (256, 32, 128, 0, 30, 700, 470, 2),    # G = 8
+    (128, 32, 128, 256, 30, 700, 200, 2),  # G = 4, at most 256 window keys
+]
+
+
+@pytest.mark.parametrize("case", SINGLE_SPLIT_GQA, ids=[str(c) for c in SINGLE_SPLIT_GQA])
+def test_fused_grouped_selection_single_split(case):
+    Hq, Hkv, d, Lp, grid, N_r, N_att, copies = case
+    L = grid * grid
+    ts = [N_att - 1, (N_att + N_r) // 2, N_r - 2, L - 1] * copies
+    Bn = len(ts)
+    say("fused grouped selection, one split", case)
+    rng = random.Random(N_att * 11 + Hq)
+    w = synth.Workload("gqasel", 1, Bn, Hq, Hkv, d, Lp, grid, grid, N_r, outlier_frac=0.01)
+    kv = synth.layer_kv(w, 0, DEV)
+    q = synth.layer_query(w, 0, DEV)
+    p = B.make_params(Lp, grid, grid, N_r, N_att)
+    s = B.make_shape(Bn, Hq, Hkv, d)
+    assert B.launch_info(p, s).max_splits == 1  # the decode kernel selects on its own
+    states, _ = c_replay_states(N_r, N_att, L, ts, Hkv, rng)
+    st0 = states_to_buffer(p, s, states, ts)
+    pos = torch.tensor(ts, dtype=torch.int32, device=DEV)
+    fb, fst = run_step(p, s, q, kv, pos, st0, True)
+    sb, sst = run_step(p, s, q, kv, pos, st0, False)
+    assert torch.equal(fst, sst)
+    assert torch.equal(fb.plan, sb.plan)
+    assert torch.equal(fb.out, sb.out)
+    assert torch.equal(fb.logits, sb.logits)
+    arrays = [request_arrays(kv, b, Lp) for b in range(Bn)]
+    forced = check_layer_vs_oracle(p, s, q, arrays, ts, states, fb.plan, fb.out, fst, fb.logits)
+    say(f"  near-tie picks adopted: {forced}")
     assert forced <= 2
