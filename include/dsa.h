@@ -31,7 +31,9 @@
  * Conventions for every call:
  *   - Pointers named d_* are DEVICE pointers owned by the caller.  The
  *     library never allocates device memory and keeps no device state between
- *     calls; buffer sizes come from the *_bytes queries.
+ *     calls; buffer sizes come from the *_bytes queries.  (The one exception
+ *     is dsa_decode_step_noalloc, whose split partials live in a fixed
+ *     per-GPU buffer inside the library.)
  *   - Calls that take a hipStream_t only enqueue work on that stream and
  *     return without synchronising; results are visible to later work on the
  *     same stream.  Calls on distinct buffers may run concurrently.
