@@ -60,7 +60,7 @@ extern "C" {
 
 #define DSA_API __attribute__((visibility("default")))
 
-#define DSA_ABI_VERSION 3
+#define DSA_ABI_VERSION 4
 
 /* ---- status codes -------------------------------------------------------- */
 typedef int32_t dsa_status;
@@ -185,19 +185,44 @@ typedef struct dsa_plan_layout {
 } dsa_plan_layout;
 
 /* Byte offsets of the arrays inside a selection-state buffer:
- *   count   int32  [B*Hkv]        skip entries stored for (b, h)
- *   flags   int32  [B*Hkv]        DSA_FLAG_* bits set by dsa_select
- *   offsets uint16 [B*Hkv][cap]   skip entries as offsets d = t - j, in the
- *                                 order Algorithm 1 appends them
+ *   count      int32  [B*Hkv]            skip entries stored for (b, h)
+ *   flags      int32  [B*Hkv]            DSA_FLAG_* bits set by dsa_select
+ *   offsets    uint16 [B*Hkv][cap]       skip entries as offsets d = t - j, in
+ *                                        the order Algorithm 1 appends them
+ *   kept_count int32  [B*Hkv][2]         slot s: k + 1 when list s below holds
+ *                                        the window's kept offsets after the
+ *                                        first k skip entries (k even in slot 0,
+ *                                        odd in slot 1); 0 when it holds none
+ *   kept       uint16 [B*Hkv][2][kept_stride]  the two lists: kept_cap
+ *                                        offsets each, largest first (oldest
+ *                                        position first)
  * cap = N_r - (N_att - S) in diagonal mode (the largest skip list of
  * Algorithm 1 over the positions after the S sinks), 0 in the other modes
- * (nothing is selected; the state buffer may then be NULL everywhere).    */
+ * (nothing is selected; the state buffer may then be NULL everywhere).
+ * kept_cap = N_att - S in diagonal mode, else 0; kept_stride = kept_cap
+ * rounded up to an even number.
+ * After k skip entries the window holds the offsets 0 .. N_att - 1 - S + k
+ * (at most N_r - 1), of which the k stored ones are skipped: N_att - S kept
+ * offsets, a function of the stored entries alone.  Where the launch rule
+ * turns them on (dsa_launch_info.kept_read), every phase-2 selection writes
+ * the list for the next step into the other slot (the new oldest offset
+ * leads, the selected one leaves), so the fused step reads its kept rows
+ * instead of rebuilding them from the skip entries, and repeating a step
+ * finds its list still there; a list that does not match the step
+ * (kept_count != k + 1) is ignored and the kept rows are rebuilt.  A caller
+ * that rewrites the skip entries itself sets kept_count to 0.  Zero-filled
+ * memory and dsa_state_reset leave no list; with kept_read = 0 the two
+ * sections are neither written nor read.                                  */
 typedef struct dsa_state_layout {
   size_t count_offset;
   size_t flags_offset;
   size_t offsets_offset;
   int32_t cap;
   size_t bytes;
+  size_t kept_count_offset;
+  size_t kept_offset;
+  int32_t kept_cap;
+  int32_t kept_stride;
 } dsa_state_layout;
 
 /* How dsa_decode_attention splits the keys (for reports and tests).  The
@@ -211,6 +236,11 @@ typedef struct dsa_launch_info {
                               the MFMA tile of grouped query heads (32 rows) */
   int32_t waves_per_group; /* waves per split workgroup (1..4; MFMA tile 1..8) */
   size_t workspace_bytes;  /* fp32 partials for the combine                 */
+  int32_t kept_read;       /* 1: selections keep the state's kept lists and
+                              dsa_decode_step reads its kept window rows from
+                              them when they match; a function of (params,
+                              shape): launches of at most 64 (request, KV
+                              head) pairs, kept_cap at most 256             */
 } dsa_launch_info;
 
 /* ---- host-only helpers (no device work) ---------------------------------- */

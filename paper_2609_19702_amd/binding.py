@@ -70,13 +70,16 @@ class PlanLayout(C.Structure):
 
 class StateLayout(C.Structure):
     _fields_ = [("count_offset", C.c_size_t), ("flags_offset", C.c_size_t),
-                ("offsets_offset", C.c_size_t), ("cap", C.c_int32), ("bytes", C.c_size_t)]
+                ("offsets_offset", C.c_size_t), ("cap", C.c_int32), ("bytes", C.c_size_t),
+                ("kept_count_offset", C.c_size_t), ("kept_offset", C.c_size_t),
+                ("kept_cap", C.c_int32), ("kept_stride", C.c_int32)]
 
 
 class LaunchInfo(C.Structure):
     _fields_ = [("rows_per_split", C.c_int32), ("max_splits", C.c_int32),
                 ("workgroups", C.c_int32), ("kernel_variant", C.c_int32),
-                ("waves_per_group", C.c_int32), ("workspace_bytes", C.c_size_t)]
+                ("waves_per_group", C.c_int32), ("workspace_bytes", C.c_size_t),
+                ("kept_read", C.c_int32)]
 
 
 # name -> (restype, argtypes); mirrors include/dsa.h
@@ -407,3 +410,15 @@ def state_views(p: Params, s: Shape, state_buf: torch.Tensor):
     flg = state_buf[L.flags_offset:L.flags_offset + 4 * pairs].view(torch.int32)
     off = state_buf[L.offsets_offset:L.offsets_offset + 2 * pairs * L.cap].view(torch.int16)
     return cnt, flg, off.view(pairs, L.cap)
+
+
+def kept_views(p: Params, s: Shape, state_buf: torch.Tensor):
+    """(tags [B*Hkv, 2] int32: k + 1 for the list of slot s after k skip
+    entries, 0 for none; lists [B*Hkv, 2, kept_stride] as int16 bit patterns
+    of the stored uint16 kept offsets, largest first)."""
+    L = state_layout(p, s)
+    pairs = s.batch * s.num_kv_heads
+    tags = state_buf[L.kept_count_offset:L.kept_count_offset + 8 * pairs].view(torch.int32)
+    n = 2 * pairs * L.kept_stride
+    lists = state_buf[L.kept_offset:L.kept_offset + 2 * n].view(torch.int16)
+    return tags.view(pairs, 2), lists.view(pairs, 2, L.kept_stride)

@@ -51,6 +51,18 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->words = d->state_cap > 0 ? (d->Nr + 31) / 32 : 0;
   if (pairs * std::max(d->plan_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
   if (pairs * std::max(d->state_cap, 1) > (int64_t(1) << 30)) return DSA_ERR_INVALID_ARG;
+  // Where it pays, every selection stores the kept list of the next step and
+  // the fused step reads its kept rows from it instead of rebuilding them
+  // from the skip entries: launches of few (request, KV head) pairs, whose
+  // time is latency, and long skip lists (build-time constants, internal.h).
+  // Elsewhere the lists are neither written nor read.
+  {
+    const int kept_cap = d->state_cap > 0 ? p->n_att - p->sinks : 0;
+    d->kept_read = kept_cap > 0 && kept_cap <= kKeptReadMax &&
+                           (pairs <= kKeptReadPairs || d->state_cap > kKeptReadCap)
+                       ? 1
+                       : 0;
+  }
 
   // plan buffer: count | flags | indices
   size_t off = 0;
@@ -63,7 +75,7 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->plan.cap = d->plan_cap;
   d->plan.bytes = off;
 
-  // state buffer: count | flags | offsets (uint16)
+  // state buffer: count | flags | offsets (uint16) | kept_count | kept (uint16)
   off = 0;
   d->state.count_offset = off;
   off = align_up(off + 4 * pairs, 256);
@@ -72,6 +84,12 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   d->state.offsets_offset = off;
   off = align_up(off + 2 * static_cast<size_t>(pairs) * d->state_cap, 256);
   d->state.cap = d->state_cap;
+  d->state.kept_cap = d->state_cap > 0 ? p->n_att - p->sinks : 0;
+  d->state.kept_stride = (d->state.kept_cap + 1) & ~1;  // even: every list starts on a 4-byte boundary
+  d->state.kept_count_offset = off;
+  off = align_up(off + 4 * 2 * pairs, 256);
+  d->state.kept_offset = off;
+  off = align_up(off + 2 * 2 * static_cast<size_t>(pairs) * d->state.kept_stride, 256);
   d->state.bytes = off;
 
   // Split configuration of the decode kernel.  A wave issues U loads of
@@ -222,6 +240,7 @@ DSA_API dsa_status dsa_get_launch_info(const dsa_params* p, const dsa_shape* s,
   out->kernel_variant = d.MF ? 100 : d.U;
   out->waves_per_group = d.NW;
   out->workspace_bytes = d.ws_bytes;
+  out->kept_read = d.kept_read;
   return DSA_OK;
 }
 
@@ -262,6 +281,7 @@ DSA_API dsa_status dsa_state_reset(const dsa_params* p, const dsa_shape* s, void
   dsa::ResetArgs a{};
   a.st_count = reinterpret_cast<int32_t*>(base + d.state.count_offset);
   a.st_flags = reinterpret_cast<int32_t*>(base + d.state.flags_offset);
+  a.st_kc = reinterpret_cast<int32_t*>(base + d.state.kept_count_offset);
   a.mask = d_req_mask;
   a.pairs = d.B * d.Hkv;
   a.Hkv = d.Hkv;
@@ -384,6 +404,10 @@ static dsa_status decode_impl(const dsa_params* p, const dsa_shape* s, const voi
       a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
       a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
       a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+      a.st_kc = reinterpret_cast<int32_t*>(sb + d.state.kept_count_offset);
+      a.st_kept = reinterpret_cast<uint16_t*>(sb + d.state.kept_offset);
+      a.kept_cap = d.state.kept_cap;
+      a.kept_read = d.kept_read;
     }
     a.plan_count = reinterpret_cast<int32_t*>(pbw + d.plan.count_offset);
     a.plan_flags = reinterpret_cast<int32_t*>(pbw + d.plan.flags_offset);
@@ -516,6 +540,11 @@ DSA_API dsa_status dsa_select(const dsa_params* p, const dsa_shape* s, const int
   a.st_count = reinterpret_cast<int32_t*>(sb + d.state.count_offset);
   a.st_flags = reinterpret_cast<int32_t*>(sb + d.state.flags_offset);
   a.st_off = reinterpret_cast<uint16_t*>(sb + d.state.offsets_offset);
+  a.st_kc = reinterpret_cast<int32_t*>(sb + d.state.kept_count_offset);
+  a.st_kept = reinterpret_cast<uint16_t*>(sb + d.state.kept_offset);
+  a.kept_cap = d.state.kept_cap;
+  a.kept_stride = d.state.kept_stride;
+  a.kept_on = d.kept_read;
   a.pairs = d.B * d.Hkv;
   a.Hq = d.Hq;
   a.Hkv = d.Hkv;

@@ -112,7 +112,7 @@ struct KvFp8 {
   }
 };
 
-constexpr int kPre = 8;  // stored skip offsets per lane loaded up front
+constexpr int kPre = 8;  // words per lane loaded ahead of the position (see PreRegs)
 
 // Keys of the (request, KV head) and the clamped decode position.
 struct RowRange {
@@ -168,48 +168,66 @@ __device__ __forceinline__ void fence_wave() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Stored count and the first kPre*64 stored offsets of a (request, KV
-// head), loaded into registers ahead of their use.
-struct StateRegs {
-  int cnt;
-  int dv[kPre];
+// What a wave that may own window rows loads ahead of the decode position
+// (kPre 16-bit values per lane), by the build:
+//   without kept lists (KL false): the first kPre*64 stored skip offsets,
+//     for the bitmap;
+//   with them (KL true): the first 256 offsets of both kept lists (slot 0
+//     for an even number of skip entries, slot 1 for an odd one; the step's
+//     slot is known once the position arrives), kPre/2 values per lane and
+//     slot.
+// Branch-free, so the loads stay in flight until the ranking uses them and
+// the waits before their first use count exactly these loads: entries past
+// the data re-read entry 0, and a wave that needs none (use = false) reads
+// a dummy address (the queries); the values are then unused.
+struct PreRegs {
+  uint32_t w[kPre];
 };
 
-// The stored offsets only (the count comes with the workgroup's other
-// per-(request, KV head) values).  Branch-free, so the loads stay in flight
-// until the ranking uses them: entries past the capacity re-read entry 0,
-// and a wave that does not need the state (use = false) reads a dummy
-// address (the queries); in both cases the values are never used.
-__device__ __forceinline__ void load_state(const DecodeArgs& a, int pair, int lane, bool use,
-                                           StateRegs& sr) {
-  const int cap = use ? a.state_cap : 0;
-  const uint16_t* off = cap > 0 ? a.st_off + static_cast<size_t>(pair) * cap
-                                : reinterpret_cast<const uint16_t*>(a.q);
+template <bool KL>
+__device__ __forceinline__ void load_pre(const DecodeArgs& a, int pair, int lane, bool use,
+                                         PreRegs& pr) {
+  constexpr int kl = KL ? 1 : 0;
+  const int stride = (a.kept_cap + 1) & ~1;
+  const int lim = use ? (kl ? a.kept_cap : a.state_cap) : 0;
+  const uint16_t* kept = a.st_kept + static_cast<size_t>(pair) * 2 * stride;
+  const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
+  const uint16_t* base = lim > 0 ? (kl ? kept : off) : reinterpret_cast<const uint16_t*>(a.q);
 #pragma unroll
   for (int i = 0; i < kPre; ++i) {
-    const int e = lane + 64 * i;
-    sr.dv[i] = off[e < cap ? e : 0];
+    const int e = lane + 64 * (i - kl * (i & (kPre / 2)));  // list mode: i mod kPre/2
+    const int so = kl * (i / (kPre / 2)) * stride;          // list mode: the slot's start
+    pr.w[i] = base[e < lim ? so + e : 0];
   }
 }
 
-__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, uint32_t* bm,
-                               const StateRegs& sr, SkipSet& ss) {
+// The skip bitmap from the first `cnt` stored offsets that the step at
+// decode position t uses.  With kept_read = 0 the first kPre*64 of them are
+// already in registers; otherwise (the kept list is missing or does not
+// fit) they are all read here.
+template <bool KL>
+__device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, int cnt,
+                               uint32_t* bm, const PreRegs& pr, SkipSet& ss) {
   const uint16_t* off = a.st_off + static_cast<size_t>(pair) * a.state_cap;
   for (int w = lane; w < a.words; w += 64) bm[w] = 0u;
   const int nvalid = min(max(t - a.Natt + 1, 0), a.state_cap);
-  int flags = sr.cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
-  const int nuse = min(max(sr.cnt, 0), nvalid);
+  int flags = cnt < nvalid ? DSA_FLAG_STATE_BEHIND : 0;
+  const int nuse = min(max(cnt, 0), nvalid);
   fence_wave();
   bool bad = false;
+  int e0 = 0;
+  if constexpr (!KL) {
 #pragma unroll
-  for (int i = 0; i < kPre; ++i) {
-    const int e = lane + 64 * i;
-    if (e < nuse) {
-      const int d = sr.dv[i];
-      if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
+    for (int i = 0; i < kPre; ++i) {
+      const int e = lane + 64 * i;
+      if (e < nuse) {
+        const int d = static_cast<int>(pr.w[i]);
+        if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
+      }
     }
+    e0 = 64 * kPre;
   }
-  for (int e = lane + 64 * kPre; e < nuse; e += 64) {
+  for (int e = lane + e0; e < nuse; e += 64) {
     const int d = off[e];
     if (d <= a.Nr - 2) atomicOr(&bm[d >> 5], 1u << (d & 31)); else bad = true;
   }
@@ -515,7 +533,7 @@ __host__ __device__ constexpr uint32_t mf_lds_bytes(int nw) {
   return mf_vt_bytes<D>(nw) + ((red + 15u) & ~15u);
 }
 
-template <class KV, int D, int G, int U, bool FUSED, bool MF>
+template <class KV, int D, int G, int U, bool FUSED, bool KL, bool MF>
 __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   constexpr int EPL = KV::kEpl;    // elements a lane loads per 16-byte access
   constexpr int LPR = D / EPL;     // lanes per row (V layout; K layout too without MF)
@@ -599,8 +617,15 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
   const int ws0 = max(r0, a.Lp);
   const int wmax = r0 + a.C > ws0 ? (r0 + a.C - ws0 + T - 1) / T : 0;
   const int per = MF ? (p0 + wmax + nwaves - 1) / nwaves : 0;
-  StateRegs sreg{};
-  sreg.cnt = has_state ? cnt_raw : 0;
+  // Fused step: the tags of the two kept lists (which numbers of skip
+  // entries they belong to), and the lists themselves for the waves that
+  // may own window rows.  Launches that keep no lists read a dummy address.
+  const int2 tags_raw =
+      FUSED && KL ? *reinterpret_cast<const int2*>(has_state
+                                                 ? static_cast<const void*>(a.st_kc + 2 * pair)
+                                                 : static_cast<const void*>(a.q))
+            : make_int2(0, 0);
+  PreRegs preld{};
   if constexpr (FUSED) {
     bool may_rank;
     if (per > 0) {
@@ -609,7 +634,7 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     } else {
       may_rank = p0 + ((wave - p0) % nwaves + nwaves) % nwaves < p0 + wmax;
     }
-    load_state(a, pair, lane, has_state && may_rank, sreg);
+    load_pre<KL>(a, pair, lane, has_state && may_rank, preld);
   }
   // Settle the scalar values here, all at once: left alone, the compiler
   // sinks each load to its first use and waits for them one at a time.
@@ -745,22 +770,50 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
       }
     }
   }
+  bool from_list = false;
   if constexpr (FUSED) {
-    // Each wave ranks the kept window rows of its own tiles (its own skip
-    // bitmap, its own slice of kp_s).
-    if (jw0 < je) {
-      build_skip_set(a, pair, lane, rr.t, bm_all + wave * a.words, sreg, ss);
-    }
-    for (int j = jw0; j < je; j += js) {
-      const int rs = wst + (j - P) * T;
-      const int re = min(rs + T, r1);
-      rank_window(lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
+    // Each wave finds the kept window rows of its own tiles (its own slice
+    // of kp_s).  From the stored kept list when it matches this step: the
+    // list for k skip entries sits in slot k % 2 tagged k + 1 (phase 2 and
+    // 3, k >= 1).  Otherwise (phase 1, the first selection step, or a state
+    // whose list is missing) from a skip bitmap of the stored offsets in
+    // the wave's own LDS slice.
+    const int kneed = min(rr.t - (a.Natt - 1), a.state_cap);
+    from_list = KL && has_state && kneed >= 1 && a.kept_cap <= 32 * kPre &&
+                ((kneed & 1) ? tags_raw.y : tags_raw.x) == kneed + 1 && cnt_raw >= kneed;
+    if (from_list) {
+      const int sl = kneed & 1;
+      for (int j = jw0; j < je; j += js) {
+        const int lo = wst + (j - P) * T - a.Lp;
+        const int hi = min(lo + a.Lp + T, r1) - a.Lp;
+        for (int r = lo + lane; r < min(hi, a.Ns); r += 64) kp_s[r - w0] = r;  // sinks
+#pragma unroll
+        for (int i = 0; i < kPre / 2; ++i) {
+          const uint32_t w0v = preld.w[i], w1v = preld.w[kPre / 2 + i];
+          const int d = static_cast<int>(sl ? w1v : w0v);
+          const int e = lane + 64 * i;
+          const int r = a.Ns + e;
+          if (e < a.kept_cap && r >= lo && r < hi) kp_s[r - w0] = rr.t - d;
+        }
+      }
+      fence_wave();
+    } else {
+      if (jw0 < je) {
+        build_skip_set<KL>(a, pair, lane, rr.t, has_state ? cnt_raw : 0, bm_all + wave * a.words,
+                       preld, ss);
+      }
+      for (int j = jw0; j < je; j += js) {
+        const int rs = wst + (j - P) * T;
+        const int re = min(rs + T, r1);
+        rank_window(lane, ss, rs - a.Lp, re - a.Lp, kp_s, w0);
+      }
     }
     // The reporting wave settles the plan flags now, so the skip set is not
-    // live through the K/V loop.
+    // live through the K/V loop (a kept list has the right count by
+    // construction).
     if (reporter) {
       rep_flags = rr.flags;
-      if (rr.t >= 0) {
+      if (rr.t >= 0 && !from_list) {
         rep_flags |= ss.flags;
         const int kept = count_kept(ss, lane);
         if (!(ss.flags & (DSA_FLAG_STATE_BEHIND | DSA_FLAG_BAD_OFFSET)) &&
@@ -1053,11 +1106,19 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
         jbest = terms_argmin<G>(lane, nwin, [&](int g, int j) { return wl_win[g * KS + j]; });
       else
         jbest = window_argmin<1>(lane, nwin, [&](int, int j) { return wl_win[j]; });
+      if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
       if (lane == 0) {
-        if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
         const int d = min(max(rr.t - kp_s[a.Ns + jbest], 0), a.Nr - 2);
         a.st_off[static_cast<size_t>(pair) * a.state_cap + ksel] = static_cast<uint16_t>(d);
         a.st_count[pair] = ksel + 1;
+      }
+      // The kept list of the next step, into the other slot.
+      if (KL && nwin == a.kept_cap) {
+        const int sl = (ksel + 1) & 1;
+        write_kept_list(lane, nwin, jbest, rr.t, a.Natt - a.Ns + ksel,
+                        [&](int r) { return kp_s[a.Ns + r]; },
+                        a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * ((a.kept_cap + 1) & ~1),
+                        a.st_kc + 2 * pair + sl, ksel + 1);
       }
     }
   }
@@ -1066,18 +1127,18 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
 // One query head per KV head: four waves per SIMD stay resident (at most
 // 128 registers), so a small sparse layer runs as a single round of
 // workgroups.  (Larger groups keep their accumulators in registers instead.)
-template <class KV, int D, int G, int U, bool FUSED>
+template <class KV, int D, int G, int U, bool FUSED, bool KL>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G == 1 ? 4 : 1, 8)))
 void decode_kernel(DecodeArgs a) {
-  decode_body<KV, D, G, U, FUSED, false>(a);
+  decode_body<KV, D, G, U, FUSED, KL, false>(a);
 }
 
 // The grouped-head (MFMA) tile holds K and V of two 32-row tiles and the
 // output blocks in registers (up to 256 of them: two waves per SIMD).
-template <class KV, int D, int G, bool FUSED>
+template <class KV, int D, int G, bool FUSED, bool KL>
 __global__ __launch_bounds__(64 * kWavesMfma) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void decode_mfma_kernel(DecodeArgs a) {
-  decode_body<KV, D, G, 2, FUSED, true>(a);
+  decode_body<KV, D, G, 2, FUSED, KL, true>(a);
 }
 
 // out = sum_s e^{m_s - M} acc_s / sum_s e^{m_s - M} l_s over the splits of
@@ -1175,16 +1236,22 @@ __global__ __launch_bounds__(kBlock + 64) void combine_select_kernel(DecodeArgs 
   const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap + a.Ns;
   const int plan_cap = a.plan_cap;
   int jbest = window_argmin<G>(lane, nwin, [&](int g, int j) { return wl[g * plan_cap + j]; });
+  if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
+  const int32_t* kept_pos = a.plan_idx + static_cast<size_t>(pair) * a.plan_cap + a.Ns;
   if (lane == 0) {
-    if (jbest < 0 || jbest >= nwin) jbest = 0;  // only for NaN logits
-    const int pos = a.plan_idx[static_cast<size_t>(pair) * a.plan_cap + a.Ns + jbest];
-    const int d = min(max(t - pos, 0), a.Nr - 2);
+    const int d = min(max(t - kept_pos[jbest], 0), a.Nr - 2);
     a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
     a.st_count[pair] = k + 1;
   }
+  if (a.kept_read && nwin == a.kept_cap) {
+    const int sl = (k + 1) & 1;
+    write_kept_list(lane, nwin, jbest, t, a.Natt - a.Ns + k, [&](int r) { return kept_pos[r]; },
+                    a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * ((a.kept_cap + 1) & ~1),
+                    a.st_kc + 2 * pair + sl, k + 1);
+  }
 }
 
-template <class KV, int D, int G, int U, bool FUSED, bool MF>
+template <class KV, int D, int G, int U, bool FUSED, bool KL, bool MF>
 void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                   hipEvent_t t1) {
   const int grid = d.B * d.Hkv * d.S;
@@ -1195,29 +1262,29 @@ void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEven
                        (FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u);
   if constexpr (MF) {
     if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED>, dim3(grid), dim3(block), lds, st,
+      hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED, KL>, dim3(grid), dim3(block), lds, st,
                             t0, t1, 0, a);
     else
-      decode_mfma_kernel<KV, D, G, FUSED><<<grid, block, lds, st>>>(a);
+      decode_mfma_kernel<KV, D, G, FUSED, KL><<<grid, block, lds, st>>>(a);
   } else {
     if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_kernel<KV, D, G, U, FUSED>, dim3(grid), dim3(block), lds, st, t0,
+      hipExtLaunchKernelGGL(decode_kernel<KV, D, G, U, FUSED, KL>, dim3(grid), dim3(block), lds, st, t0,
                             t1, 0, a);
     else
-      decode_kernel<KV, D, G, U, FUSED><<<grid, block, lds, st>>>(a);
+      decode_kernel<KV, D, G, U, FUSED, KL><<<grid, block, lds, st>>>(a);
   }
 }
 
-template <class KV, int D, int G, bool FUSED>
+template <class KV, int D, int G, bool FUSED, bool KL>
 hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                      hipEvent_t t1) {
   // With several splits the stop event goes to the combine, so a timed call
   // covers every kernel it launches.
   const bool split = d.S > 1;
   if constexpr (uses_mfma_tile(G))
-    launch_split<KV, D, G, 2, FUSED, true>(d, a, st, t0, split ? nullptr : t1);
+    launch_split<KV, D, G, 2, FUSED, KL, true>(d, a, st, t0, split ? nullptr : t1);
   else
-    launch_split<KV, D, G, unroll_of(G), FUSED, false>(d, a, st, t0, split ? nullptr : t1);
+    launch_split<KV, D, G, unroll_of(G), FUSED, KL, false>(d, a, st, t0, split ? nullptr : t1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
   if (FUSED) {
@@ -1238,14 +1305,14 @@ hipError_t launch_dg(const Derived& d, const DecodeArgs& a, hipStream_t st, hipE
   return hipGetLastError();
 }
 
-template <class KV, int D, bool FUSED>
+template <class KV, int D, bool FUSED, bool KL>
 hipError_t launch_d(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                     hipEvent_t t1) {
   switch (d.G) {
-    case 1: return launch_dg<KV, D, 1, FUSED>(d, a, st, t0, t1);
-    case 2: return launch_dg<KV, D, 2, FUSED>(d, a, st, t0, t1);
-    case 4: return launch_dg<KV, D, 4, FUSED>(d, a, st, t0, t1);
-    default: return launch_dg<KV, D, 8, FUSED>(d, a, st, t0, t1);
+    case 1: return launch_dg<KV, D, 1, FUSED, KL>(d, a, st, t0, t1);
+    case 2: return launch_dg<KV, D, 2, FUSED, KL>(d, a, st, t0, t1);
+    case 4: return launch_dg<KV, D, 4, FUSED, KL>(d, a, st, t0, t1);
+    default: return launch_dg<KV, D, 8, FUSED, KL>(d, a, st, t0, t1);
   }
 }
 
@@ -1254,11 +1321,17 @@ hipError_t launch_d(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEv
 template <class KV>
 hipError_t launch_kv(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEvent_t t0,
                      hipEvent_t t1, bool fused) {
+  // The fused step has two builds: with the kept lists of the selection
+  // state (launch rule kept_read) and without, so launches that keep no
+  // lists carry none of their code.
+  if (fused && a.kept_read)
+    return d.D == 64 ? launch_d<KV, 64, true, true>(d, a, st, t0, t1)
+                     : launch_d<KV, 128, true, true>(d, a, st, t0, t1);
   if (fused)
-    return d.D == 64 ? launch_d<KV, 64, true>(d, a, st, t0, t1)
-                     : launch_d<KV, 128, true>(d, a, st, t0, t1);
-  return d.D == 64 ? launch_d<KV, 64, false>(d, a, st, t0, t1)
-                   : launch_d<KV, 128, false>(d, a, st, t0, t1);
+    return d.D == 64 ? launch_d<KV, 64, true, false>(d, a, st, t0, t1)
+                     : launch_d<KV, 128, true, false>(d, a, st, t0, t1);
+  return d.D == 64 ? launch_d<KV, 64, false, false>(d, a, st, t0, t1)
+                   : launch_d<KV, 128, false, false>(d, a, st, t0, t1);
 }
 
 }  // namespace

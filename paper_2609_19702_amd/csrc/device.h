@@ -138,6 +138,23 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 namespace dsa {
 
+// The window's kept offsets for the step after a phase-2 selection (the
+// list a selection state keeps, see dsa_state_layout): this step's kept
+// window rank r (0 <= r < nwin, ascending positions pos(r)) has offset
+// t - pos(r); the selected rank jsel leaves, and the offset the window gains
+// at the next step, first_off, leads.  Largest offset first.  Lane 0 then
+// tags the list with k_next + 1 (k_next: the skip entries stored after this
+// selection).  Called by a whole wave.
+template <typename Pos>
+__device__ __forceinline__ void write_kept_list(int lane, int nwin, int jsel, int t, int first_off,
+                                                Pos pos, uint16_t* kept, int32_t* tag,
+                                                int k_next) {
+  if (lane == 0) kept[0] = static_cast<uint16_t>(first_off);
+  for (int r = lane; r < nwin; r += 64)
+    if (r != jsel) kept[r < jsel ? r + 1 : r] = static_cast<uint16_t>(t - pos(r));
+  if (lane == 0) *tag = k_next + 1;
+}
+
 // (value, index) minimum with ties to the smaller index.
 __device__ __forceinline__ void argmin_merge(float& v, int& j, float v2, int j2) {
   if (v2 < v || (v2 == v && j2 < j)) {

@@ -29,6 +29,7 @@ struct Derived {
   int NW;         // waves per decode workgroup (1..kWaves), bf16 caches
   int NW_fp8;     // the same for fp8 caches (tiles of twice the rows)
   bool MF;        // grouped query heads on the MFMA tile (uses_mfma_tile(G))
+  int kept_read;  // 1: selections store kept lists and the fused step reads its kept rows from them
   size_t ws_bytes;
 };
 
@@ -82,6 +83,13 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d);
 #ifndef DSA_TUNE_MFMA_WAVES_DENSE
 #define DSA_TUNE_MFMA_WAVES_DENSE 2  // the same in dense mode (long rows, many workgroups)
 #endif
+#ifndef DSA_TUNE_KEPT_READ_PAIRS
+#define DSA_TUNE_KEPT_READ_PAIRS 64  // selection states keep kept lists for the fused step in
+#endif                               // launches of at most this many (request, KV head) pairs ...
+#ifndef DSA_TUNE_KEPT_READ_CAP
+#define DSA_TUNE_KEPT_READ_CAP 512   // ... or with skip lists longer than this (ranking exposed or
+#endif                               // long; measured: large launches with short lists lose
+                                     // 0.3-1 us per layer to the list stores)
 #ifndef DSA_TUNE_VALU_GQA
 #define DSA_TUNE_VALU_GQA 0  // 1: grouped query heads on the vector-ALU tile instead of MFMA
 #endif
@@ -104,6 +112,9 @@ constexpr int kSplitKbDense128 = DSA_TUNE_SPLIT_KB_DENSE_128;
 constexpr int kSplitKbDenseMfma = DSA_TUNE_SPLIT_KB_DENSE_MFMA;
 constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
 constexpr int kMinWorkgroupsSparse = DSA_TUNE_MIN_WGS_SPARSE;
+constexpr int kKeptReadPairs = DSA_TUNE_KEPT_READ_PAIRS;
+constexpr int kKeptReadCap = DSA_TUNE_KEPT_READ_CAP;
+constexpr int kKeptReadMax = 256;    // kept offsets per list the fused step loads ahead (4 per lane)
 static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
 static_assert(kMaxFusedSplitMfma % 64 == 0 && kMaxFusedSplitMfma <= 1024, "fused split rows");
 // Rows of one sparse-mode split at most, by tile.
@@ -168,7 +179,10 @@ struct DecodeArgs {
   int32_t* plan_count;
   int32_t* plan_flags;
   int32_t* plan_idx;
-  int Nr, Natt, state_cap, words;
+  int32_t* st_kc;      // kept lists: tags [pairs][2] (k + 1, or 0) and lists (fused step)
+  uint16_t* st_kept;
+  int Nr, Natt, state_cap, words, kept_cap;
+  int kept_read;       // 1: kept lists are stored by the selection and read by the fused step
 };
 
 struct SelectArgs {
@@ -179,12 +193,16 @@ struct SelectArgs {
   int32_t* st_count;
   int32_t* st_flags;
   uint16_t* st_off;
-  int pairs, Hq, Hkv, G, Ldec, Nr, Natt, Ns, plan_cap, state_cap;
+  int32_t* st_kc;      // kept lists: tags [pairs][2] (k + 1, or 0) and lists
+  uint16_t* st_kept;
+  int pairs, Hq, Hkv, G, Ldec, Nr, Natt, Ns, plan_cap, state_cap, kept_cap, kept_stride;
+  int kept_on;         // 1: the state's kept lists are maintained (the launch rule of the fused step)
 };
 
 struct ResetArgs {
   int32_t* st_count;
   int32_t* st_flags;
+  int32_t* st_kc;
   const int32_t* mask;
   int pairs, Hkv;
 };

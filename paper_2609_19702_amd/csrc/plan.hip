@@ -127,6 +127,8 @@ __global__ __launch_bounds__(256) void reset_kernel(ResetArgs a) {
   if (a.mask && a.mask[pair / a.Hkv] == 0) return;
   a.st_count[pair] = 0;
   a.st_flags[pair] = 0;
+  a.st_kc[2 * pair] = 0;
+  a.st_kc[2 * pair + 1] = 0;
 }
 
 }  // namespace

@@ -42,12 +42,18 @@ __global__ __launch_bounds__(kBlock) void select_kernel(SelectArgs a) {
   const float* wl = a.wlog + (static_cast<size_t>(b) * a.Hq + kvh * G) * a.plan_cap + a.Ns;
   const int plan_cap = a.plan_cap;
   int jbest = window_argmin<G>(lane, nw, [&](int g, int j) { return wl[g * plan_cap + j]; });
+  if (jbest < 0 || jbest >= nw) jbest = 0;  // only for NaN logits
+  const int32_t* kept_pos = a.idx + static_cast<size_t>(pair) * a.plan_cap + a.Ns;
   if (lane == 0) {
-    if (jbest < 0 || jbest >= nw) jbest = 0;  // only for NaN logits
-    const int pos = a.idx[static_cast<size_t>(pair) * a.plan_cap + a.Ns + jbest];
-    const int d = min(max(t - pos, 0), a.Nr - 2);
+    const int d = min(max(t - kept_pos[jbest], 0), a.Nr - 2);
     a.st_off[static_cast<size_t>(pair) * a.state_cap + k] = static_cast<uint16_t>(d);
     a.st_count[pair] = k + 1;
+  }
+  if (a.kept_on && nw == a.kept_cap) {
+    const int sl = (k + 1) & 1;
+    write_kept_list(lane, nw, jbest, t, a.Natt - a.Ns + k, [&](int r) { return kept_pos[r]; },
+                    a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * a.kept_stride,
+                    a.st_kc + 2 * pair + sl, k + 1);
   }
 }
 

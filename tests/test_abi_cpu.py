@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(B.SIGNATURES), "binding and header disagree"
-    assert B.abi_version() == 3
+    assert B.abi_version() == 4
 
 
 def test_status_strings():

@@ -3,7 +3,13 @@ calls (``dsa_plan -> dsa_decode_attention -> dsa_select``): plan, window
 logits, output and selection state must be identical bit for bit, with one
 split or several, at phase-1, phase-2 and phase-3 positions, with unused
 slots and with grouped query heads.  A tiny decode trajectory driven only by
-the fused step stays in lockstep with the oracle."""
+the fused step stays in lockstep with the oracle.
+
+The fused step reads its kept window rows from the kept list the previous
+selection stored (when it matches the step) instead of rebuilding them from
+the skip entries: with the lists removed it must give the same plan, logits,
+outputs and stored offsets, and every stored list must equal the window
+part of the plan, as offsets from the decode position, largest first."""
 
 import math
 
@@ -72,6 +78,94 @@ def test_fused_equals_separate_calls(case):
         for b in range(Bn):
             n = int(rcnt[b * Hkv])
             assert torch.equal(lg_f[b, :, :n], lg_r[b, :, :n]), (li, b)
+
+
+@pytest.mark.parametrize("case", CASES[:4], ids=[c[0] for c in CASES[:4]])
+def test_fused_kept_list_equals_rebuild(case):
+    name, nl, Bn, Hq, Hkv, d, Lp, gh, gw, win = case
+    w = synth.Workload(name, nl, Bn, Hq, Hkv, d, Lp, gh, gw, win, sparsity_permille=900,
+                       outlier_frac=0.01)
+    L = gh * gw
+    rng = np.random.default_rng(11)
+    pos = rng.integers(0, L, Bn).tolist()
+    p0 = B.params_from_sparsity(Lp, gh, gw, win, 900)
+    pos[0] = p0.n_att - 1          # first phase-2 step: no list yet
+    pos[1] = p0.n_att              # first step that has one
+    pos[2] = p0.window - 2         # last phase-2 step
+    pos[3] = p0.window - 1         # first phase-3 step
+    bt = workload.make_batch(w, positions=pos)
+    workload.build_histories(bt)
+    p, s = bt.p, bt.s
+    lay = B.state_layout(p, s)
+    assert lay.kept_cap == p.n_att - p.sinks
+    reads = B.launch_info(p, s).kept_read
+    assert reads == (Bn * Hkv <= 64)  # the launches of few pairs read the lists
+    say(name, "kept_cap", lay.kept_cap, "reads lists", reads, "positions", pos)
+    states = [Lr.bufs.state.clone() for Lr in bt.layers]
+    # every list the histories stored matches the plan of its step
+    workload.step(bt, fused=True)
+    torch.cuda.synchronize()
+    ref = [(Lr.bufs.out.clone(), Lr.bufs.state.clone(), Lr.bufs.plan.clone(), Lr.bufs.logits.clone())
+           for Lr in bt.layers]
+    used = 0
+    for Lr, st0 in zip(bt.layers, states):
+        tags, lists = B.kept_views(p, s, st0)
+        if not reads:  # launches that keep no lists never write them
+            assert not tags.any()
+            continue
+        cnt, _, idx = B.plan_views(p, s, Lr.bufs.plan)
+        for pair in range(Bn * Hkv):
+            t = pos[pair // Hkv]
+            k = min(t - (p.n_att - 1), lay.cap)
+            if k < 1:
+                continue
+            sl = k & 1
+            assert int(tags[pair, sl]) == k + 1, (pair, t, k)
+            used += 1
+            got = (lists[pair, sl, :lay.kept_cap].to(torch.int64) & 0xFFFF).tolist()
+            n = int(cnt[pair])
+            want = [t - int(j) for j in idx[pair, p.sinks:n].tolist()]
+            assert got == want, (pair, t)
+    assert used > 0 or not reads
+    # the same step with every list removed: the kept rows are rebuilt
+    for Lr, st in zip(bt.layers, states):
+        st2 = st.clone()
+        tags, _ = B.kept_views(p, s, st2)
+        tags.zero_()
+        Lr.bufs.state.copy_(st2)
+        Lr.bufs.out.fill_(float("nan"))
+        Lr.bufs.plan.fill_(0x5A)
+        Lr.bufs.logits.fill_(float("nan"))
+    workload.step(bt, fused=True)
+    torch.cuda.synchronize()
+    for li, (Lr, (o, st, pl, lg)) in enumerate(zip(bt.layers, ref)):
+        assert torch.equal(Lr.bufs.out, o), li
+        cnt, flg, idx = B.plan_views(p, s, Lr.bufs.plan)
+        rcnt, rflg, ridx = B.plan_views(p, s, pl)
+        assert torch.equal(cnt, rcnt) and torch.equal(flg, rflg), li
+        for pair in range(Bn * Hkv):
+            n = int(rcnt[pair])
+            assert torch.equal(idx[pair, :n], ridx[pair, :n]), (li, pair)
+        lg_a, lg_r = Lr.bufs.logits.view(Bn, Hq, -1), lg.view(Bn, Hq, -1)
+        for b in range(Bn):
+            n = int(rcnt[b * Hkv])
+            assert torch.equal(lg_a[b, :, :n], lg_r[b, :, :n]), (li, b)
+        a_cnt, a_flg, a_off = B.state_views(p, s, Lr.bufs.state)
+        r_cnt, r_flg, r_off = B.state_views(p, s, st)
+        assert torch.equal(a_cnt, r_cnt) and torch.equal(a_flg, r_flg) and torch.equal(a_off, r_off)
+        # the list each selection stored for the next step (other slot)
+        a_tags, a_lists = B.kept_views(p, s, Lr.bufs.state)
+        r_tags, r_lists = B.kept_views(p, s, st)
+        if not reads:
+            assert not a_tags.any() and not r_tags.any()
+            continue
+        for pair in range(Bn * Hkv):
+            t = pos[pair // Hkv]
+            k = t - (p.n_att - 1)
+            if 0 <= k < lay.cap:
+                sl = (k + 1) & 1
+                assert int(a_tags[pair, sl]) == k + 2 == int(r_tags[pair, sl]), (li, pair)
+                assert torch.equal(a_lists[pair, sl, :lay.kept_cap], r_lists[pair, sl, :lay.kept_cap])
 
 
 def test_fused_tiny_trajectory():
