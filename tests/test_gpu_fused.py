@@ -107,6 +107,13 @@ def test_fused_kept_list_equals_rebuild(case):
     torch.cuda.synchronize()
     ref = [(Lr.bufs.out.clone(), Lr.bufs.state.clone(), Lr.bufs.plan.clone(), Lr.bufs.logits.clone())
            for Lr in bt.layers]
+    # the same step again on the state it left (as a benchmark repeats it): its
+    # list is still in its slot, and every result is the same
+    workload.step(bt, fused=True)
+    torch.cuda.synchronize()
+    for li, (Lr, (o, st, pl, lg)) in enumerate(zip(bt.layers, ref)):
+        assert torch.equal(Lr.bufs.out, o) and torch.equal(Lr.bufs.state, st), li
+        assert torch.equal(Lr.bufs.plan, pl), li
     used = 0
     for Lr, st0 in zip(bt.layers, states):
         tags, lists = B.kept_views(p, s, st0)
@@ -181,6 +188,8 @@ def test_fused_tiny_trajectory():
     k64, v64 = k[0].double().cpu().numpy(), v[0].double().cpu().numpy()
     Q64 = T["Q"].double().numpy()
     states = ostep.new_states(H, N_r, N_att)
+    assert B.launch_info(p, s).kept_read == 1  # every step after the first selection reads a list
+    cap = B.state_layout(p, s).cap
     forced = 0
     for t in range(256):
         pos = torch.tensor([t], dtype=torch.int32, device=DEV)
@@ -188,6 +197,10 @@ def test_fused_tiny_trajectory():
                       bufs.state, bufs.plan, scale, bufs.out, bufs.logits, bufs.workspace)
         cnt, flg, idx = (x.cpu().numpy() for x in B.plan_views(p, s, bufs.plan))
         scnt, sflg, soff = offsets_from_buffer(p, s, bufs.state)
+        kk = t - (N_att - 1)
+        if 0 <= kk < cap:  # this step selected: the next step's list is stored, tagged
+            tags, _ = B.kept_views(p, s, bufs.state)
+            assert (tags[:, (kk + 1) & 1] == kk + 2).all(), t
 
         def decide(kvh, t_, idx_, j_ref, sigma):
             nonlocal forced
