@@ -80,7 +80,15 @@ def test_fused_equals_separate_calls(case):
             assert torch.equal(lg_f[b, :, :n], lg_r[b, :, :n]), (li, b)
 
 
-@pytest.mark.parametrize("case", CASES[:4], ids=[c[0] for c in CASES[:4]])
+LIST_CASES = CASES[:4] + [
+    # many (request, KV head) pairs and skip lists of 770-864 entries: lists on,
+    # three splits per request (the combine stores the next step's list)
+    ("wide_gqa2", 1, 33, 4, 2, 64, 16, 40, 40, 1024),
+    ("wide_mha", 1, 70, 1, 1, 64, 8, 36, 36, 900),
+]
+
+
+@pytest.mark.parametrize("case", LIST_CASES, ids=[c[0] for c in LIST_CASES])
 def test_fused_kept_list_equals_rebuild(case):
     name, nl, Bn, Hq, Hkv, d, Lp, gh, gw, win = case
     w = synth.Workload(name, nl, Bn, Hq, Hkv, d, Lp, gh, gw, win, sparsity_permille=900,
@@ -98,8 +106,12 @@ def test_fused_kept_list_equals_rebuild(case):
     p, s = bt.p, bt.s
     lay = B.state_layout(p, s)
     assert lay.kept_cap == p.n_att - p.sinks
-    reads = B.launch_info(p, s).kept_read
-    assert reads == (Bn * Hkv <= 64)  # the launches of few pairs read the lists
+    info = B.launch_info(p, s)
+    reads = info.kept_read
+    # lists for launches of few pairs or long skip lists, of at most 256 kept offsets
+    assert reads == ((Bn * Hkv <= 64 or lay.cap > 512) and lay.kept_cap <= 256)
+    if name.startswith("wide"):
+        assert reads and info.max_splits > 1
     say(name, "kept_cap", lay.kept_cap, "reads lists", reads, "positions", pos)
     states = [Lr.bufs.state.clone() for Lr in bt.layers]
     # every list the histories stored matches the plan of its step
