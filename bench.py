@@ -256,6 +256,53 @@ def timed_steps(bt, steps, mode, graph):
     return start.elapsed_time(end) / steps
 
 
+def step_distribution(graph, steps):
+    """Median, 10th and 90th percentile (ms) of single graph-replayed steps,
+    each between its own pair of events; a pass of its own after the timed
+    steps, which it does not change."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record()
+        graph.replay()
+        b.record()
+    torch.cuda.synchronize()
+    return percentiles([a.elapsed_time(b) for a, b in evs])
+
+
+def percentiles(xs):
+    q = sorted(xs)
+
+    def at(f):  # linear interpolation between order statistics
+        x = f * (len(q) - 1)
+        i = int(x)
+        return q[i] + (q[min(i + 1, len(q) - 1)] - q[i]) * (x - i)
+
+    return {"median": at(0.5), "p10": at(0.1), "p90": at(0.9), "n": len(q)}
+
+
+def gpu_clocks():
+    """Current shader and memory clocks as rocm-smi reports them (a read-only
+    query; None where it is missing or fails)."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi")
+    if exe is None:
+        return None
+    try:
+        r = subprocess.run([exe, "--showclocks", "--json"], capture_output=True, text=True,
+                           timeout=30)
+        cards = json.loads(r.stdout)
+    except (subprocess.SubprocessError, OSError, ValueError):
+        return None
+    for card, fields in sorted(cards.items()):
+        if isinstance(fields, dict):
+            return {"card": card, **{k.rstrip(":"): v for k, v in fields.items() if "clk" in k}}
+    return None
+
+
 def spin_cycles_per_ms():
     """Rate of torch's spin kernel (``torch.cuda._sleep``), measured."""
     import torch
@@ -494,6 +541,9 @@ def main():
     torch.cuda.synchronize()
     ms = {m: timed_steps(bt, args.steps, m, graphs[m]) for m in modes}
     launch = {m: kernel_times(bt, args.steps, m, prefill=not args.eager) for m in modes}
+    dist = None
+    if graphs.get("fused") is not None:
+        dist = step_distribution(graphs["fused"], args.steps)
     if args.only:
         print(json.dumps({"only": args.only, "ms_per_step": ms[args.only],
                           "decode_launch_us": statistics.fmean(launch[args.only]) * 1e3}))
@@ -579,7 +629,13 @@ def main():
             # every kernel of one layer in the timed replays, launch gaps included
             "layer_us_in_step": ms_sparse * 1e3 / n_layers,
             "launch_us": mean_launch_ms * 1e3, "source_hash": src_hash,
+            "launch_us_dist": {k: (v * 1e3 if k != "n" else v)
+                               for k, v in percentiles(launch_sparse).items()},
         },
+        # single graph-replayed steps, timed apart from the steps above
+        "step_ms_dist": dist,
+        # read once the timed work is over (a query during it would perturb it)
+        "gpu_clocks_after_run": gpu_clocks(),
         "cpu_baseline": base,
         "paper_context": PAPER_CONTEXT,
     }

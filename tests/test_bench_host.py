@@ -7,6 +7,8 @@ import os
 import subprocess
 import sys
 
+import numpy as np
+
 import bench
 from paper_2609_19702_amd import synth
 
@@ -66,3 +68,13 @@ def test_traffic_only_for_the_current_kernel_source(tmp_path, monkeypatch):
     assert bench.traffic_for("absent", h) is None
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.json"))
     assert bench.traffic_for("w_now", h) is None
+
+
+def test_step_percentiles_match_numpy():
+    rng = np.random.default_rng(3)
+    for n in (1, 2, 7, 20, 101):
+        xs = rng.exponential(1.0, n).tolist()
+        got = bench.percentiles(xs)
+        for k, f in (("median", 50), ("p10", 10), ("p90", 90)):
+            assert abs(got[k] - float(np.percentile(xs, f))) <= 1e-12 * max(1.0, max(xs)), (n, k)
+        assert got["n"] == n
