@@ -376,8 +376,10 @@ DSA_API dsa_status dsa_decode_attention_timed(const dsa_params* p, const dsa_sha
  * with bit-identical plan, window logits, output and selection state, the
  * way the paper's own kernel fuses the index gather and the window argmin
  * into the attention (section 5.1, "Implementation").  Every decode
- * workgroup rebuilds the kept set of its (request, KV head) from d_state;
- * when one split covers a (request, KV head) it also runs the phase-2
+ * workgroup rebuilds the kept set of its (request, KV head) from d_state,
+ * or reads it from the state's kept list where the launch keeps them
+ * (dsa_launch_info.kept_read); when one split covers a (request, KV head)
+ * it also runs the phase-2
  * argmin and appends the skip entry, otherwise a second kernel merges the
  * splits and selects.  In dense mode it is dsa_decode_attention and d_state,
  * d_plan and d_window_logits are not used.
