@@ -59,12 +59,20 @@ def test_state_reset_mask():
     cnt, flg, _ = B.state_views(p, s, st)
     cnt[:] = 7
     flg[:] = 3
+    tags, lists = B.kept_views(p, s, st)
+    tags[:] = 9
+    lists[:] = 5
     st = st.to(DEV)
     mask = torch.tensor([1, 0, 1, 0], dtype=torch.int32, device=DEV)
     B.state_reset(p, s, st, mask)
     cnt, flg, _ = B.state_views(p, s, st.cpu())
     assert cnt.tolist() == [0, 0, 7, 7, 0, 0, 7, 7]
     assert flg.tolist() == [0, 0, 3, 3, 0, 0, 3, 3]
+    # the kept lists of the reset requests are dropped (both tags 0); the
+    # others keep theirs; the list contents themselves are not touched
+    tags, lists = B.kept_views(p, s, st.cpu())
+    assert tags.tolist() == [[0, 0]] * 2 + [[9, 9]] * 2 + [[0, 0]] * 2 + [[9, 9]] * 2
+    assert (lists == 5).all()
 
 
 def test_two_streams_concurrently():
