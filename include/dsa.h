@@ -240,7 +240,8 @@ typedef struct dsa_launch_info {
                               dsa_decode_step reads its kept window rows from
                               them when they match; a function of (params,
                               shape): launches of at most 64 (request, KV
-                              head) pairs, kept_cap at most 256             */
+                              head) pairs with kept_cap <= 512, or with
+                              cap > 512 and kept_cap <= 256                 */
 } dsa_launch_info;
 
 /* ---- host-only helpers (no device work) ---------------------------------- */

@@ -58,10 +58,9 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   // Elsewhere the lists are neither written nor read.
   {
     const int kept_cap = d->state_cap > 0 ? p->n_att - p->sinks : 0;
-    d->kept_read = kept_cap > 0 && kept_cap <= kKeptReadMax &&
-                           (pairs <= kKeptReadPairs || d->state_cap > kKeptReadCap)
-                       ? 1
-                       : 0;
+    const bool few = pairs <= kKeptReadPairs && kept_cap <= kKeptReadMax;
+    const bool longs = d->state_cap > kKeptReadCap && kept_cap <= kKeptReadMaxWide;
+    d->kept_read = kept_cap > 0 && (few || longs) ? 1 : 0;
   }
 
   // plan buffer: count | flags | indices

@@ -779,10 +779,11 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
     // whose list is missing) from a skip bitmap of the stored offsets in
     // the wave's own LDS slice.
     const int kneed = min(rr.t - (a.Natt - 1), a.state_cap);
-    from_list = KL && has_state && kneed >= 1 && a.kept_cap <= 32 * kPre &&
+    from_list = KL && has_state && kneed >= 1 &&
                 ((kneed & 1) ? tags_raw.y : tags_raw.x) == kneed + 1 && cnt_raw >= kneed;
     if (from_list) {
       const int sl = kneed & 1;
+      const uint16_t* list = a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * ((a.kept_cap + 1) & ~1);
       for (int j = jw0; j < je; j += js) {
         const int lo = wst + (j - P) * T - a.Lp;
         const int hi = min(lo + a.Lp + T, r1) - a.Lp;
@@ -795,6 +796,10 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
           const int r = a.Ns + e;
           if (e < a.kept_cap && r >= lo && r < hi) kp_s[r - w0] = rr.t - d;
         }
+        // entries past the ones loaded ahead (lists longer than 32 * kPre)
+        const int e_hi = min(a.kept_cap, hi - a.Ns);
+        for (int e = max(32 * kPre, lo - a.Ns) + lane; e < e_hi; e += 64)
+          kp_s[a.Ns + e - w0] = rr.t - static_cast<int>(list[e]);
       }
       fence_wave();
     } else {

@@ -114,7 +114,8 @@ constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
 constexpr int kMinWorkgroupsSparse = DSA_TUNE_MIN_WGS_SPARSE;
 constexpr int kKeptReadPairs = DSA_TUNE_KEPT_READ_PAIRS;
 constexpr int kKeptReadCap = DSA_TUNE_KEPT_READ_CAP;
-constexpr int kKeptReadMax = 256;    // kept offsets per list the fused step loads ahead (4 per lane)
+constexpr int kKeptReadMax = 512;    // longest kept list the fused step reads (the first 256 loaded ahead) ...
+constexpr int kKeptReadMaxWide = 256;  // ... in launches of few pairs; this long in the others
 static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
 static_assert(kMaxFusedSplitMfma % 64 == 0 && kMaxFusedSplitMfma <= 1024, "fused split rows");
 // Rows of one sparse-mode split at most, by tile.

@@ -85,6 +85,10 @@ LIST_CASES = CASES[:4] + [
     # three splits per request (the combine stores the next step's list)
     ("wide_gqa2", 1, 33, 4, 2, 64, 16, 40, 40, 1024),
     ("wide_mha", 1, 70, 1, 1, 64, 8, 36, 36, 900),
+    # few pairs with kept lists longer than the 256 offsets loaded ahead
+    # (N_att 360 and 410; several splits per request)
+    ("long_lists", 1, 40, 2, 1, 64, 16, 60, 60, 2048),
+    ("long_lists_gqa4", 1, 12, 16, 4, 128, 0, 64, 64, 1500),
 ]
 
 
@@ -109,9 +113,12 @@ def test_fused_kept_list_equals_rebuild(case):
     info = B.launch_info(p, s)
     reads = info.kept_read
     # lists for launches of few pairs or long skip lists, of at most 256 kept offsets
-    assert reads == ((Bn * Hkv <= 64 or lay.cap > 512) and lay.kept_cap <= 256)
+    assert reads == ((Bn * Hkv <= 64 and lay.kept_cap <= 512)
+                     or (lay.cap > 512 and lay.kept_cap <= 256))
     if name.startswith("wide"):
         assert reads and info.max_splits > 1
+    if name.startswith("long"):
+        assert reads and lay.kept_cap > 256
     say(name, "kept_cap", lay.kept_cap, "reads lists", reads, "positions", pos)
     states = [Lr.bufs.state.clone() for Lr in bt.layers]
     # every list the histories stored matches the plan of its step
