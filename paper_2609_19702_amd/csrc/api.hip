@@ -84,7 +84,8 @@ dsa_status derive(const dsa_params* p, const dsa_shape* s, Derived* d) {
   off = align_up(off + 2 * static_cast<size_t>(pairs) * d->state_cap, 256);
   d->state.cap = d->state_cap;
   d->state.kept_cap = d->state_cap > 0 ? p->n_att - p->sinks : 0;
-  d->state.kept_stride = (d->state.kept_cap + 1) & ~1;  // even: every list starts on a 4-byte boundary
+  // even, so every list starts on a 4-byte boundary
+  d->state.kept_stride = (d->state.kept_cap + 1) & ~1;
   d->state.kept_count_offset = off;
   off = align_up(off + 4 * 2 * pairs, 256);
   d->state.kept_offset = off;

@@ -202,9 +202,9 @@ __device__ __forceinline__ void load_pre(const DecodeArgs& a, int pair, int lane
 }
 
 // The skip bitmap from the first `cnt` stored offsets that the step at
-// decode position t uses.  With kept_read = 0 the first kPre*64 of them are
-// already in registers; otherwise (the kept list is missing or does not
-// fit) they are all read here.
+// decode position t uses.  In the build without kept lists (KL false) the
+// first kPre*64 of them are already in registers; in the other one (the
+// step's kept list is missing) they are all read here.
 template <bool KL>
 __device__ void build_skip_set(const DecodeArgs& a, int pair, int lane, int t, int cnt,
                                uint32_t* bm, const PreRegs& pr, SkipSet& ss) {
@@ -783,7 +783,8 @@ __device__ __forceinline__ void decode_body(const DecodeArgs& a) {
                 ((kneed & 1) ? tags_raw.y : tags_raw.x) == kneed + 1 && cnt_raw >= kneed;
     if (from_list) {
       const int sl = kneed & 1;
-      const uint16_t* list = a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * ((a.kept_cap + 1) & ~1);
+      const uint16_t* list =
+          a.st_kept + (static_cast<size_t>(pair) * 2 + sl) * ((a.kept_cap + 1) & ~1);
       for (int j = jw0; j < je; j += js) {
         const int lo = wst + (j - P) * T - a.Lp;
         const int hi = min(lo + a.Lp + T, r1) - a.Lp;
@@ -1267,14 +1268,14 @@ void launch_split(const Derived& d, const DecodeArgs& a, hipStream_t st, hipEven
                        (FUSED ? static_cast<uint32_t>(sizeof(uint32_t) * nw * a.words) : 0u);
   if constexpr (MF) {
     if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED, KL>, dim3(grid), dim3(block), lds, st,
-                            t0, t1, 0, a);
+      hipExtLaunchKernelGGL(decode_mfma_kernel<KV, D, G, FUSED, KL>, dim3(grid), dim3(block), lds,
+                            st, t0, t1, 0, a);
     else
       decode_mfma_kernel<KV, D, G, FUSED, KL><<<grid, block, lds, st>>>(a);
   } else {
     if (t0 || t1)
-      hipExtLaunchKernelGGL(decode_kernel<KV, D, G, U, FUSED, KL>, dim3(grid), dim3(block), lds, st, t0,
-                            t1, 0, a);
+      hipExtLaunchKernelGGL(decode_kernel<KV, D, G, U, FUSED, KL>, dim3(grid), dim3(block), lds,
+                            st, t0, t1, 0, a);
     else
       decode_kernel<KV, D, G, U, FUSED, KL><<<grid, block, lds, st>>>(a);
   }

@@ -114,8 +114,10 @@ constexpr int kMinWorkgroups = DSA_TUNE_MIN_WGS;
 constexpr int kMinWorkgroupsSparse = DSA_TUNE_MIN_WGS_SPARSE;
 constexpr int kKeptReadPairs = DSA_TUNE_KEPT_READ_PAIRS;
 constexpr int kKeptReadCap = DSA_TUNE_KEPT_READ_CAP;
-constexpr int kKeptReadMax = 512;    // longest kept list the fused step reads (the first 256 loaded ahead) ...
-constexpr int kKeptReadMaxWide = 256;  // ... in launches of few pairs; this long in the others
+// Longest kept list the fused step reads (the first 256 offsets are loaded
+// ahead of the position): in launches of few pairs, and in the others.
+constexpr int kKeptReadMax = 512;
+constexpr int kKeptReadMaxWide = 256;
 static_assert(kMaxFusedSplit % 64 == 0 && kMaxFusedSplit <= 1024, "fused split rows");
 static_assert(kMaxFusedSplitMfma % 64 == 0 && kMaxFusedSplitMfma <= 1024, "fused split rows");
 // Rows of one sparse-mode split at most, by tile.
@@ -197,7 +199,7 @@ struct SelectArgs {
   int32_t* st_kc;      // kept lists: tags [pairs][2] (k + 1, or 0) and lists
   uint16_t* st_kept;
   int pairs, Hq, Hkv, G, Ldec, Nr, Natt, Ns, plan_cap, state_cap, kept_cap, kept_stride;
-  int kept_on;         // 1: the state's kept lists are maintained (the launch rule of the fused step)
+  int kept_on;         // 1: the state's kept lists are kept (the fused step's launch rule)
 };
 
 struct ResetArgs {
