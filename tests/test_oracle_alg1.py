@@ -145,3 +145,26 @@ def test_invalid_parameters():
         alg1.HeadState(4, 5)
     with pytest.raises(ValueError):
         alg1.HeadState(4, 0)
+
+
+@pytest.mark.parametrize("N_r", [2, 3, 6, 11, 24])
+def test_next_kept_offsets_follow_from_the_selection(N_r):
+    """The property the selection state's kept lists rest on, on the literal
+    Algorithm 1: after a phase-2 selection at step t (k entries before it),
+    the kept offsets of step t + 1, oldest first, are the new oldest offset
+    N_att + k followed by step t's kept offsets without the selected one;
+    once the selections are over, the kept offsets stay the same."""
+    rng = random.Random(77 + N_r)
+    for N_att in range(1, N_r + 1):
+        for rep in range(10):
+            T = 2 * N_r + 5
+            recs = alg1.run(N_r, N_att, T, alg1.uniform([rng.randrange(1 << 30) for _ in range(N_r)]))
+            for a, b in zip(recs, recs[1:]):
+                t = a.t
+                offs_t = [t - j for j in a.idx]
+                offs_next = [t + 1 - j for j in b.idx]
+                if a.selected is not None:
+                    k = t - (N_att - 1)
+                    assert offs_next == [N_att + k] + [d for d in offs_t if d != t - a.selected]
+                elif t >= N_r - 1:
+                    assert offs_next == offs_t
