@@ -72,6 +72,9 @@ def parse():
     ap.add_argument("--trajectory", action="store_true",
                     help="time a whole image: every request decodes positions 0 .. H*W-1 over "
                          "every layer (fused step, and dense mode), one JSON line")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="with --trajectory: requests per image batch instead of the workload's "
+                         "(1: single-image latency)")
     ap.add_argument("--cells", default=None,
                     help="with --sweep: comma-separated substrings of the cell names to run")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
@@ -439,6 +442,8 @@ def run_trajectory(args):
     from paper_2609_19702_amd import binding as B
     from paper_2609_19702_amd import synth, workload
     w = synth.WORKLOADS[args.workload].with_(positions="last")
+    if args.batch:
+        w = w.with_(batch=args.batch, name=f"{w.name}_b{args.batch}")
     t0 = time.time()
     bt = workload.make_batch(w)
     L_dec = w.decode_len
@@ -447,7 +452,8 @@ def run_trajectory(args):
     res = {"metric": "whole-image decode attention time (all positions, all layers)",
            "workload": f"{w.name}_like", "layers": len(bt.layers), "batch": w.batch,
            "positions": L_dec, "window": bt.p.window, "n_att": bt.p.n_att,
-           "launch": "hip_graph per position"}
+           "launch": "hip_graph per position",
+           "kept_lists": B.launch_info(bt.p, bt.s).kept_read}
     for mode in ("fused", "dense"):
         for L in bt.layers:
             B.state_reset(bt.p, bt.s, L.bufs.state)
